@@ -1,0 +1,228 @@
+"""Throughput of the split-FFT convolution hot path on one MI355X.
+
+Default workload: the 56x56x256 layer with a 5x5 kernel, batch 16,
+256 -> 256 channels, stride 1, 'same' padding, fp32, tile T = 28 (FFT size
+L = 32), overlap-save; synthetic seeded inputs (ReLU of N(0,1)) and
+He-normal weights, resident in device memory before timing starts.
+
+A step is one pass of the hot path over the batch: forward patch
+transform -> per-bin contraction -> inverse transform with placement (the
+three kernels of fftsplit_conv2d, launched through the stage entry points
+so that each can be timed with events on the stream it runs on).  The
+filter spectra are computed once, before timing (a once-per-layer cost).
+
+Prints one JSON line (see the fields below).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix, TFLOP/s
+
+DEFAULT_CONFIG = "c4_56x256_k5"
+DEFAULT_TILE = 28
+
+
+def algorithmic_counts(layer, info):
+    """Algorithmic bytes/flops of each kernel per launch (one batch).
+
+    forward : read x once + write the patch spectra once
+    contract: 8 flops per complex multiply-add, over every stored bin,
+              padded patch and padded output channel the kernel computes
+    inverse : read the output spectra once + write y once
+    """
+    F, ntp, coutp = info.bins, info.tiles_padded, info.cout_padded
+    nt = info.tiles
+    x_bytes = 4 * layer.n * layer.cin * layer.h * layer.w
+    y_bytes = 4 * layer.n * layer.cout * layer.h * layer.w
+    return {
+        "forward_bytes": x_bytes + 8 * F * layer.cin * nt,
+        "contract_flops": 8 * F * layer.cin * layer.cout * nt,
+        "contract_bytes": 8 * F * (layer.cin * nt + layer.cin * layer.cout + layer.cout * nt),
+        "inverse_bytes": 8 * F * layer.cout * nt + y_bytes,
+    }
+
+
+def cpu_baseline(layer, x, w, b, tile, budget_s=12.0):
+    """Time the CPU oracle's split-FFT convolution on a bounded sample of
+    the batch (whole images, until about `budget_s` seconds have passed)."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
+    except Exception:  # pragma: no cover
+        blas_threads = 1
+    cores = len(os.sched_getaffinity(0))
+    done, t_total = 0, 0.0
+    while done < layer.n and t_total < budget_s:
+        t0 = time.perf_counter()
+        oracle.split_conv(x[done:done + 1], w, b, t=tile, mode="os")
+        t_total += time.perf_counter() - t0
+        done += 1
+    per_img = t_total / done
+    gflops = layer.direct_flops / layer.n / per_img / 1e9
+    return {"value": round(gflops, 3), "unit": "GFLOP/s", "cores": int(min(cores, blas_threads)),
+            "kind": "oracle",
+            "sample": f"oracle.split_conv (float64 numpy, naive-DFT split, overlap-save) on {done} of "
+                      f"{layer.n} images, {t_total:.1f} s; {1.0 / per_img:.3f} images/s; "
+                      f"{cores} host cores visible, BLAS threads {blas_threads}"}
+
+
+def load_traffic(kernel_tag):
+    """HBM traffic per launch from a committed rocprofv3 --pmc summary, if it
+    was taken on the current kernel sources; otherwise None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(kernel_tag)
+        if not rec:
+            return None
+        from paper_2003_12621_amd.build import source_digest
+        if rec.get("source_digest") != source_digest():
+            return None
+        return rec.get("bytes_per_launch")
+    except Exception:
+        return None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default=DEFAULT_CONFIG)
+    ap.add_argument("--tile", type=int, default=None)
+    ap.add_argument("--mode", default="os", choices=["os", "oaa"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-parity", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for {args.gpus}); the multi-GPU "
+              "sharding of the path is a design note, not an implementation.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2003_12621_amd as fs
+    from workloads import CONFIGS, make_config
+
+    cfg = CONFIGS[args.config]
+    layer = cfg["layer"]
+    tile = args.tile if args.tile is not None else (DEFAULT_TILE if args.config == DEFAULT_CONFIG else cfg["tiles"][-1])
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+
+    x, w, b = make_config(args.config)
+    plan = fs.Plan(layer.n, layer.cin, layer.h, layer.w, layer.cout, layer.k, tile=tile, mode=args.mode,
+                   bias=b is not None, device=0)
+    info = plan.info
+    xd = torch.from_numpy(x).to(dev)
+    wd = torch.from_numpy(w).to(dev)
+    bd = None if b is None else torch.from_numpy(b).to(dev)
+    wspec = plan.transform_weights(wd)
+    ws = plan.new_workspace()
+    y = plan.new_output()
+    torch.cuda.synchronize()
+
+    def step(evs=None):
+        if evs is not None:
+            evs[0].record()
+        plan.forward(xd, ws)
+        if evs is not None:
+            evs[1].record()
+        plan.contract(wspec, ws)
+        if evs is not None:
+            evs[2].record()
+        plan.inverse(ws, bias=bd, out=y)
+        if evs is not None:
+            evs[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+
+    fwd = [e[0].elapsed_time(e[1]) for e in evs]
+    con = [e[1].elapsed_time(e[2]) for e in evs]
+    inv = [e[2].elapsed_time(e[3]) for e in evs]
+    total_ms = evs[0][0].elapsed_time(evs[-1][3])
+    ms_per_step = total_ms / args.steps
+    avg = lambda v: sum(v) / len(v)  # noqa: E731
+
+    counts = algorithmic_counts(layer, info)
+    fwd_gbs = counts["forward_bytes"] / (avg(fwd) * 1e-3) / 1e9
+    inv_gbs = counts["inverse_bytes"] / (avg(inv) * 1e-3) / 1e9
+    con_tfs = counts["contract_flops"] / (avg(con) * 1e-3) / 1e12
+    value = layer.direct_flops / (ms_per_step * 1e-3) / 1e9
+
+    # Parity of the timed output against the oracle on sampled output channels.
+    parity = None
+    if not args.no_parity:
+        import oracle
+        rng = np.random.default_rng(99)
+        sel = np.sort(rng.choice(layer.cout, size=4, replace=False))
+        imgs = slice(0, min(layer.n, 4))
+        ref = oracle.direct_xcorr2d(x[imgs], w[sel], None if b is None else b[sel])
+        got = y.cpu().numpy()[imgs][:, sel].astype(np.float64)
+        parity = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+
+    traffic = load_traffic(f"contract_{args.config}_T{tile}_{args.mode}")
+    out = {
+        "metric": "effective direct-conv GFLOP/s",
+        "value": round(value, 1),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{args.config}: n={layer.n} cin={layer.cin} {layer.h}x{layer.w} "
+                               f"cout={layer.cout} k={layer.k} stride1 same",
+                   "tile": info.tile, "nfft": info.nfft, "mode": args.mode, "tiles": info.tiles,
+                   "bins": info.bins},
+        "images_per_s": round(layer.n / (ms_per_step * 1e-3), 1),
+        "roofline": {"bound": "mfma", "kernel": "contract (per-bin complex Cin->Cout product)",
+                     "achieved": round(con_tfs, 2), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(con_tfs / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": traffic},
+        "stages": {
+            "forward": {"ms": round(avg(fwd), 4), "GB/s": round(fwd_gbs, 1),
+                        "frac_hbm": round(fwd_gbs / HBM_PEAK_GBS, 4), "bytes": counts["forward_bytes"]},
+            "contract": {"ms": round(avg(con), 4), "TFLOP/s": round(con_tfs, 2),
+                         "frac_mfma": round(con_tfs / FP32_MFMA_PEAK_TFLOPS, 4),
+                         "flops": counts["contract_flops"], "bytes": counts["contract_bytes"]},
+            "inverse": {"ms": round(avg(inv), 4), "GB/s": round(inv_gbs, 1),
+                        "frac_hbm": round(inv_gbs / HBM_PEAK_GBS, 4), "bytes": counts["inverse_bytes"]},
+        },
+        "wall_s_timed": round(t_wall, 4),
+        "parity_rel_l2": parity,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(layer, x, w, b, tile)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,184 @@
+/*
+ * fftsplit.h -- C ABI of the split-FFT 2-D convolution library for AMD
+ * MI355X (gfx950).
+ *
+ * Method: Chitsaz et al., "Acceleration of Convolutional Neural Network Using
+ * FFT-Based Split Convolutions" (arXiv:2003.12621), Section 3.1.  A stride-1
+ * 'same' convolution layer (CNN cross-correlation, odd K x K kernel, K//2
+ * zeros of padding) is computed by
+ *   1. splitting each input plane into T x T patches (eq. 4),
+ *   2. padding each patch to L x L, L = T + K - 1 (eqs. 5-6),
+ *   3. a 2-D real FFT of every padded patch, and of every zero-padded filter
+ *      (eq. 8, done once per layer by fftsplit_transform_weights),
+ *   4. the entry-wise product of patch and filter spectra (eq. 9), summed
+ *      over input channels: per frequency bin a Cin -> Cout complex matrix
+ *      product batched over patches,
+ *   5. an inverse FFT per (patch, output channel), crop and concatenation of
+ *      the valid T x T tile (eq. 10 and the text after it) -- or, with
+ *      FFTSPLIT_OVERLAP_ADD, zero-padded patches whose L x L results are
+ *      overlap-added (the discipline of Section 2, Fig. 1, at tile size T),
+ *   6. optional bias and ReLU, fused into the inverse stage.
+ *
+ * Result: y = relu?(conv2d(x, w, bias, stride=1, padding=K//2)) with
+ * PyTorch's cross-correlation convention, in fp32.
+ *
+ * Conventions for every entry point:
+ *   - Tensors are fp32 and densely packed (C order).  Pointers marked
+ *     "device" are device addresses on the plan's device; "host" pointers
+ *     are host memory.  Device buffers must be 16-byte aligned.
+ *   - The caller owns every buffer.  The library never allocates device
+ *     memory; a plan owns host memory only.
+ *   - Work is enqueued asynchronously on the given stream (0 = the null
+ *     stream).  The return status covers argument checks and launch errors;
+ *     a fault inside a kernel surfaces at the caller's next synchronisation.
+ *   - No C++ exception crosses this ABI.  On any status other than
+ *     FFTSPLIT_SUCCESS, fftsplit_last_error() returns a message for the
+ *     calling thread and nothing has been enqueued.
+ *   - A plan is immutable after creation and may be used from several
+ *     threads and streams at once, as long as each concurrent call has its
+ *     own workspace and output.
+ */
+#ifndef FFTSPLIT_H
+#define FFTSPLIT_H
+
+#include <stddef.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct fftsplit_plan_s* fftsplit_plan_t;   /* opaque, host-side */
+
+typedef enum {
+    FFTSPLIT_SUCCESS = 0,
+    FFTSPLIT_ERROR_INVALID_VALUE = 1,        /* bad dimension, NULL/misaligned pointer, aliasing */
+    FFTSPLIT_ERROR_NOT_SUPPORTED = 2,        /* even K, stride != 1, pad != K/2, L not in {8,16,32} */
+    FFTSPLIT_ERROR_INSUFFICIENT_WORKSPACE = 3,
+    FFTSPLIT_ERROR_DEVICE = 4,               /* a HIP runtime call or kernel launch failed */
+    FFTSPLIT_ERROR_ARCH = 5                  /* the device is not gfx950 */
+} fftsplit_status_t;
+
+/* Problem flags. */
+enum {
+    FFTSPLIT_OVERLAP_SAVE = 0,   /* halo'd patches, crop + concatenate (Section 3.1); default */
+    FFTSPLIT_OVERLAP_ADD  = 1,   /* zero-padded patches, overlap-add of the L x L results */
+    FFTSPLIT_BIAS         = 2,   /* add bias[co] in the inverse stage */
+    FFTSPLIT_RELU         = 4    /* apply max(., 0) after the bias */
+};
+
+/* The layer, as the paper states the problem: batch n, channels cin -> cout,
+ * an h x w input, a k x k filter, the patch (tile) size, stride 1 and zero
+ * padding of k/2 (Section 2, eq. 1; Section 3.1). */
+typedef struct {
+    int n, cin, h, w, cout, k;
+    int tile;        /* T; 0 lets the plan choose among L = 8, 16, 32 */
+    int stride;      /* must be 1 */
+    int pad;         /* must be k/2 ('same') */
+    unsigned flags;  /* FFTSPLIT_* flags above */
+} fftsplit_problem_t;
+
+/* What a plan decided.  Spectra are complex64 (re, im float pairs).
+ *
+ * Frequency bins: the 2-D real transform of an L x L patch has L*(L/2+1)
+ * bins (k1 in [0,L), k2 in [0,L/2]); columns k2 = 0 and k2 = L/2 are
+ * Hermitian in k1, so only their k1 <= L/2 halves are kept, leaving
+ * bins = L*L/2 + 2.  Bin index f enumerates
+ *   f = (k2-1)*L + k1                 for k2 in [1, L/2-1], k1 in [0, L)
+ *   f = L*(L/2-1) + k1                for k2 = 0,   k1 in [0, L/2]
+ *   f = L*(L/2-1) + L/2+1 + k1        for k2 = L/2, k1 in [0, L/2]
+ *
+ * Patch index t = (img * tiles_h + a) * tiles_w + b for the patch whose
+ * top-left output pixel is (a*T, b*T); t in [tiles, tiles_padded) are zero
+ * padding.
+ *
+ * Layouts (all complex64, innermost index last):
+ *   weight spectra  W[bins][cin][cout_padded]        (wspec, wspec_bytes)
+ *       = conj(DFT of w[co][ci] zero-padded top-left to L x L) / L^2,
+ *         zero for co >= cout
+ *   patch spectra   X[bins][cin][tiles_padded]       (workspace + xspec_offset)
+ *   output spectra  Y[bins][cout_padded][tiles_padded] (workspace + yspec_offset)
+ * The DFT is unnormalised, exp(-2 pi i (m k1 + q k2) / L). */
+typedef struct {
+    int tile;            /* T */
+    int nfft;            /* L = T + k - 1 */
+    int tiles_h, tiles_w;/* ceil(h/T), ceil(w/T) */
+    int tiles;           /* n * tiles_h * tiles_w */
+    int tiles_padded;    /* tiles rounded up to the contraction's tile granularity */
+    int bins;            /* L*L/2 + 2 */
+    int cout_padded;     /* cout rounded up to the contraction's tile granularity */
+    unsigned flags;
+    size_t wspec_bytes;
+    size_t workspace_bytes;
+    size_t xspec_offset, xspec_bytes;
+    size_t yspec_offset, yspec_bytes;
+    size_t aux_offset, aux_bytes;   /* overlap-add seam partials (0 for overlap-save) */
+} fftsplit_plan_info_t;
+
+/* Validate `prob` (host) and create a plan for `device` (a HIP ordinal).
+ * Queries the device: its gcnArchName must start with "gfx950", else
+ * FFTSPLIT_ERROR_ARCH.  With prob->tile == 0 the plan picks T from a cost
+ * model over L = 8, 16, 32; the environment variable FFTSPLIT_TILE forces a
+ * tile size.  No device memory is touched.  *out is set only on success. */
+fftsplit_status_t fftsplit_plan(const fftsplit_problem_t* prob, int device, fftsplit_plan_t* out);
+
+/* As fftsplit_plan, but for a named architecture string (host-only, no HIP
+ * call).  The resulting plan can be queried but not executed: the entry
+ * points that launch work return FFTSPLIT_ERROR_INVALID_VALUE for it. */
+fftsplit_status_t fftsplit_plan_for_arch(const fftsplit_problem_t* prob, const char* arch,
+                                         fftsplit_plan_t* out);
+
+fftsplit_status_t fftsplit_plan_info(fftsplit_plan_t plan, fftsplit_plan_info_t* out /* host */);
+
+/* Frees a plan's host memory.  NULL is ignored. */
+void fftsplit_plan_destroy(fftsplit_plan_t plan);
+
+/* Eq. (8) and the filter half of eq. (9), once per layer:
+ * w (device) [cout][cin][k][k] -> wspec (device, info.wspec_bytes).  The
+ * spectra are evaluated in double precision and rounded once to fp32. */
+fftsplit_status_t fftsplit_transform_weights(fftsplit_plan_t plan, const float* w, void* wspec,
+                                             hipStream_t stream);
+
+/* The hot path, Section 3.1 steps 1-6:
+ *   x (device) [n][cin][h][w], wspec from fftsplit_transform_weights,
+ *   bias (device) [cout] or NULL (required iff FFTSPLIT_BIAS),
+ *   y (device) [n][cout][h][w] (must not overlap x),
+ *   workspace (device) of at least info.workspace_bytes.
+ * Enqueues the forward patch transform, the per-bin contraction and the
+ * inverse transform with placement on `stream`. */
+fftsplit_status_t fftsplit_conv2d(fftsplit_plan_t plan, const float* x, const void* wspec,
+                                  const float* bias, float* y, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream);
+
+/* The three stages of fftsplit_conv2d, separately (same arguments and
+ * workspace layout; running them in order is exactly fftsplit_conv2d).
+ * They exist for stage-by-stage testing and per-kernel timing.
+ *   forward:  x -> patch spectra at workspace + xspec_offset (eqs. 4-6, FFT)
+ *   contract: patch spectra, wspec -> output spectra at yspec_offset (eq. 9)
+ *   inverse:  output spectra -> y, with crop/concatenate or overlap-add,
+ *             bias and ReLU (eq. 10). */
+fftsplit_status_t fftsplit_forward(fftsplit_plan_t plan, const float* x, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+fftsplit_status_t fftsplit_contract(fftsplit_plan_t plan, const void* wspec, void* workspace,
+                                    size_t workspace_bytes, hipStream_t stream);
+fftsplit_status_t fftsplit_inverse(fftsplit_plan_t plan, const float* bias, float* y,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* 2x2, stride-2 max-pool (floor), used between the stages of a VGG-16
+ * stack; not part of the method.  x (device) [n][c][h][w] ->
+ * y (device) [n][c][h/2][w/2].  x and y must not overlap. */
+fftsplit_status_t fftsplit_maxpool2x2(const float* x, float* y, int n, int c, int h, int w,
+                                      hipStream_t stream);
+
+/* Static description of a status code. */
+const char* fftsplit_status_string(fftsplit_status_t status);
+
+/* Detail of the calling thread's last failure (empty string if none).
+ * Valid until the thread's next call into the library. */
+const char* fftsplit_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FFTSPLIT_H */

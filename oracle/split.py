@@ -90,22 +90,28 @@ def patch_spectra(x, t: int, k: int, mode: str = "os") -> np.ndarray:
 
 
 def hadamard_channel_sum(xs, ws) -> np.ndarray:
-    """Step 4: Z[n,a,b,co] = sum_ci Xs[n,a,b,ci] * conj(Ws[co,ci]) entry-wise (eq. 9).
+    """Step 4: Z[..., co, bins] = sum_ci Xs[..., ci, bins] * conj(Ws[co, ci, bins]) (eq. 9).
 
-    xs: [n, th, tw, cin, L, L] patch spectra; ws: [cout, cin, L, L] filter
-    spectra.  Returns [n, th, tw, cout, L, L].
+    xs: [..., cin, *bins] patch spectra (normally [n, th, tw, cin, L, L]);
+    ws: [cout, cin, *bins] filter spectra with the same trailing bin axes.
+    Returns [..., cout, *bins].
     """
     xs = np.asarray(xs, dtype=np.complex128)
     ws = np.asarray(ws, dtype=np.complex128)
-    n, th, tw, cin, L, _ = xs.shape
-    cout = ws.shape[0]
-    # For each frequency bin (k, l): the [patches x cin] matrix of patch
-    # spectra times the [cin x cout] matrix of conjugated filter spectra.
-    # Entry (patch, co) is sum_ci Xs[patch, ci, k, l] * conj(Ws[co, ci, k, l]).
-    xb = xs.reshape(n * th * tw, cin, L, L).transpose(2, 3, 0, 1)   # [L, L, P, cin]
-    wb = np.conj(ws).transpose(2, 3, 1, 0)                          # [L, L, cin, cout]
-    zb = np.matmul(xb, wb)                                          # [L, L, P, cout]
-    return np.ascontiguousarray(zb.transpose(2, 3, 0, 1)).reshape(n, th, tw, cout, L, L)
+    cout, cin = ws.shape[:2]
+    bins = ws.shape[2:]
+    lead = xs.shape[:xs.ndim - len(bins) - 1]
+    if xs.shape[len(lead)] != cin or xs.shape[len(lead) + 1:] != bins:
+        raise ValueError("patch and filter spectra do not match")
+    nb = int(np.prod(bins)) if bins else 1
+    npatch = int(np.prod(lead)) if lead else 1
+    # For each frequency bin: the [patches x cin] matrix of patch spectra
+    # times the [cin x cout] matrix of conjugated filter spectra.  Entry
+    # (patch, co) is sum_ci Xs[patch, ci, bin] * conj(Ws[co, ci, bin]).
+    xb = xs.reshape(npatch, cin, nb).transpose(2, 0, 1)          # [bins, P, cin]
+    wb = np.conj(ws).reshape(cout, cin, nb).transpose(2, 1, 0)   # [bins, cin, cout]
+    zb = np.matmul(xb, wb)                                       # [bins, P, cout]
+    return np.ascontiguousarray(zb.transpose(1, 2, 0)).reshape(*lead, cout, *bins)
 
 
 def inverse_place(z_spec, h: int, w: int, t: int, k: int, mode: str = "os",

@@ -1,0 +1,274 @@
+"""Python binding of libfftsplit: split-FFT 2-D convolution on MI355X (gfx950).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels behind the C ABI declared in include/fftsplit.h.  PyTorch supplies
+device memory (``torch.empty(..., device='cuda')``) and the stream
+(``torch.cuda.current_stream()``).  If the built library is missing the
+import of the native entry points fails loudly; there is no fallback.
+
+    import paper_2003_12621_amd as fs
+    plan = fs.Plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28)
+    wspec = plan.transform_weights(w)          # once per layer
+    y = plan.conv2d(x, wspec)                  # the hot path
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libfftsplit.so")
+
+SUCCESS = 0
+ERROR_INVALID_VALUE = 1
+ERROR_NOT_SUPPORTED = 2
+ERROR_INSUFFICIENT_WORKSPACE = 3
+ERROR_DEVICE = 4
+ERROR_ARCH = 5
+
+OVERLAP_SAVE = 0
+OVERLAP_ADD = 1
+BIAS = 2
+RELU = 4
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int), ("cin", ctypes.c_int), ("h", ctypes.c_int), ("w", ctypes.c_int),
+                ("cout", ctypes.c_int), ("k", ctypes.c_int), ("tile", ctypes.c_int), ("stride", ctypes.c_int),
+                ("pad", ctypes.c_int), ("flags", ctypes.c_uint)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("tile", ctypes.c_int), ("nfft", ctypes.c_int), ("tiles_h", ctypes.c_int),
+                ("tiles_w", ctypes.c_int), ("tiles", ctypes.c_int), ("tiles_padded", ctypes.c_int),
+                ("bins", ctypes.c_int), ("cout_padded", ctypes.c_int), ("flags", ctypes.c_uint),
+                ("wspec_bytes", ctypes.c_size_t), ("workspace_bytes", ctypes.c_size_t),
+                ("xspec_offset", ctypes.c_size_t), ("xspec_bytes", ctypes.c_size_t),
+                ("yspec_offset", ctypes.c_size_t), ("yspec_bytes", ctypes.c_size_t),
+                ("aux_offset", ctypes.c_size_t), ("aux_bytes", ctypes.c_size_t)]
+
+
+class FftsplitError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} ({detail})")
+
+
+_lib = None
+
+# Every function the header declares, with its ctypes signature.
+_SIGNATURES = {
+    "fftsplit_plan": (ctypes.c_int, [ctypes.POINTER(Problem), ctypes.c_int, ctypes.POINTER(ctypes.c_void_p)]),
+    "fftsplit_plan_for_arch": (ctypes.c_int, [ctypes.POINTER(Problem), ctypes.c_char_p,
+                                              ctypes.POINTER(ctypes.c_void_p)]),
+    "fftsplit_plan_info": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(PlanInfo)]),
+    "fftsplit_plan_destroy": (None, [ctypes.c_void_p]),
+    "fftsplit_transform_weights": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                                  ctypes.c_void_p]),
+    "fftsplit_conv2d": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "fftsplit_forward": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                        ctypes.c_void_p]),
+    "fftsplit_contract": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                         ctypes.c_void_p]),
+    "fftsplit_inverse": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_size_t, ctypes.c_void_p]),
+    "fftsplit_maxpool2x2": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                           ctypes.c_int, ctypes.c_int, ctypes.c_void_p]),
+    "fftsplit_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "fftsplit_last_error": (ctypes.c_char_p, []),
+}
+
+
+def lib():
+    """Load libfftsplit.so (built in-tree by ``paper_2003_12621_amd.build``)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2003_12621_amd.build`")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().fftsplit_status_string(status).decode()
+
+
+def last_error() -> str:
+    return lib().fftsplit_last_error().decode()
+
+
+def _check(status: int, where: str):
+    if status != SUCCESS:
+        raise FftsplitError(status, where, last_error())
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_handle(device) -> ctypes.c_void_p:
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _dev_tensor(t, name: str, dtype=None, numel: Optional[int] = None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) torch tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def problem(n, cin, h, w, cout, k, tile=0, mode="os", bias=False, relu=False, stride=1, pad=None) -> Problem:
+    flags = (OVERLAP_ADD if mode == "oaa" else OVERLAP_SAVE) | (BIAS if bias else 0) | (RELU if relu else 0)
+    if mode not in ("os", "oaa"):
+        raise ValueError("mode must be 'os' or 'oaa'")
+    return Problem(n, cin, h, w, cout, k, tile, stride, k // 2 if pad is None else pad, flags)
+
+
+class Plan:
+    """A validated layer plan (host-side).  See fftsplit.h for every field."""
+
+    def __init__(self, n, cin, h, w, cout, k, tile=0, mode="os", bias=False, relu=False, device=None,
+                 arch: Optional[str] = None, stride=1, pad=None):
+        self.prob = problem(n, cin, h, w, cout, k, tile, mode, bias, relu, stride, pad)
+        handle = ctypes.c_void_p()
+        if arch is not None:
+            _check(lib().fftsplit_plan_for_arch(ctypes.byref(self.prob), arch.encode(), ctypes.byref(handle)),
+                   "fftsplit_plan_for_arch")
+            self.device = None
+        else:
+            torch = _torch()
+            dev = torch.device("cuda", torch.cuda.current_device() if device is None else int(device))
+            _check(lib().fftsplit_plan(ctypes.byref(self.prob), dev.index, ctypes.byref(handle)), "fftsplit_plan")
+            self.device = dev
+        self._h = handle
+        info = PlanInfo()
+        _check(lib().fftsplit_plan_info(self._h, ctypes.byref(info)), "fftsplit_plan_info")
+        self.info = info
+        self.n, self.cin, self.h, self.w, self.cout, self.k = n, cin, h, w, cout, k
+        self.mode, self.has_bias, self.relu = mode, bias, relu
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.fftsplit_plan_destroy(h)
+            self._h = None
+
+    # -- shapes ---------------------------------------------------------
+    @property
+    def tile(self) -> int:
+        return self.info.tile
+
+    @property
+    def nfft(self) -> int:
+        return self.info.nfft
+
+    def new_workspace(self):
+        torch = _torch()
+        return torch.empty(self.info.workspace_bytes, dtype=torch.uint8, device=self.device)
+
+    def new_output(self):
+        torch = _torch()
+        return torch.empty((self.n, self.cout, self.h, self.w), dtype=torch.float32, device=self.device)
+
+    # -- entry points ---------------------------------------------------
+    def transform_weights(self, w, out=None):
+        """Filter spectra (complex64 stored as float32 pairs), once per layer."""
+        torch = _torch()
+        wp = _dev_tensor(w, "w", torch.float32, self.cout * self.cin * self.k * self.k)
+        if out is None:
+            out = torch.empty(self.info.wspec_bytes // 4, dtype=torch.float32, device=self.device)
+        if out.numel() * out.element_size() < self.info.wspec_bytes:
+            raise ValueError("wspec buffer too small")
+        _check(lib().fftsplit_transform_weights(self._h, wp, _dev_tensor(out, "wspec"), _stream_handle(self.device)),
+               "fftsplit_transform_weights")
+        return out
+
+    def conv2d(self, x, wspec, bias=None, out=None, workspace=None):
+        torch = _torch()
+        xp = _dev_tensor(x, "x", torch.float32, self.n * self.cin * self.h * self.w)
+        out = self.new_output() if out is None else out
+        yp = _dev_tensor(out, "y", torch.float32, self.n * self.cout * self.h * self.w)
+        ws = self.new_workspace() if workspace is None else workspace
+        bp = None if bias is None else _dev_tensor(bias, "bias", torch.float32, self.cout)
+        _check(lib().fftsplit_conv2d(self._h, xp, _dev_tensor(wspec, "wspec"), bp, yp, _dev_tensor(ws, "workspace"),
+                                     ws.numel() * ws.element_size(), _stream_handle(self.device)),
+               "fftsplit_conv2d")
+        return out
+
+    def forward(self, x, workspace):
+        torch = _torch()
+        xp = _dev_tensor(x, "x", torch.float32, self.n * self.cin * self.h * self.w)
+        _check(lib().fftsplit_forward(self._h, xp, _dev_tensor(workspace, "workspace"),
+                                      workspace.numel() * workspace.element_size(), _stream_handle(self.device)),
+               "fftsplit_forward")
+
+    def contract(self, wspec, workspace):
+        _check(lib().fftsplit_contract(self._h, _dev_tensor(wspec, "wspec"), _dev_tensor(workspace, "workspace"),
+                                       workspace.numel() * workspace.element_size(), _stream_handle(self.device)),
+               "fftsplit_contract")
+
+    def inverse(self, workspace, bias=None, out=None):
+        torch = _torch()
+        out = self.new_output() if out is None else out
+        yp = _dev_tensor(out, "y", torch.float32, self.n * self.cout * self.h * self.w)
+        bp = None if bias is None else _dev_tensor(bias, "bias", torch.float32, self.cout)
+        _check(lib().fftsplit_inverse(self._h, bp, yp, _dev_tensor(workspace, "workspace"),
+                                      workspace.numel() * workspace.element_size(), _stream_handle(self.device)),
+               "fftsplit_inverse")
+        return out
+
+    # -- views of the workspace (complex64), for stage-level tests -------
+    def xspec_view(self, workspace):
+        i = self.info
+        raw = workspace[i.xspec_offset:i.xspec_offset + i.xspec_bytes]
+        return raw.view(_torch().complex64).view(i.bins, self.cin, i.tiles_padded)
+
+    def yspec_view(self, workspace):
+        i = self.info
+        raw = workspace[i.yspec_offset:i.yspec_offset + i.yspec_bytes]
+        return raw.view(_torch().complex64).view(i.bins, i.cout_padded, i.tiles_padded)
+
+    def wspec_view(self, wspec):
+        i = self.info
+        return wspec.view(_torch().complex64)[: i.bins * self.cin * i.cout_padded].view(i.bins, self.cin,
+                                                                                         i.cout_padded)
+
+
+def maxpool2x2(x, out=None):
+    """2x2 stride-2 max-pool (floor) on an NCHW float32 CUDA tensor."""
+    torch = _torch()
+    n, c, h, w = x.shape
+    out = torch.empty((n, c, h // 2, w // 2), dtype=torch.float32, device=x.device) if out is None else out
+    xp = _dev_tensor(x, "x", torch.float32)
+    yp = _dev_tensor(out, "y", torch.float32, n * c * (h // 2) * (w // 2))
+    _check(lib().fftsplit_maxpool2x2(xp, yp, n, c, h, w, _stream_handle(x.device)), "fftsplit_maxpool2x2")
+    return out
+
+
+def bin_coords(L: int):
+    """(k1, k2) of each stored bin, in the library's bin order (fftsplit.h)."""
+    h2 = L // 2
+    coords = []
+    for k2 in range(1, h2):
+        for k1 in range(L):
+            coords.append((k1, k2))
+    for k1 in range(h2 + 1):
+        coords.append((k1, 0))
+    for k1 in range(h2 + 1):
+        coords.append((k1, h2))
+    return coords

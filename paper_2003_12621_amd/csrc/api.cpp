@@ -1,0 +1,172 @@
+// Entry points that enqueue work: argument checks, device selection, kernel
+// launch sequence and HIP-error mapping.
+#include <cstdint>
+#include <string>
+
+#include "fftsplit_internal.hpp"
+
+using namespace fftsplit;
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool overlap(const void* a, size_t an, const void* b, size_t bn) {
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+    return a0 < b0 + bn && b0 < a0 + an;
+}
+
+// Makes the plan's device current for the duration of a call.
+class DeviceGuard {
+  public:
+    explicit DeviceGuard(int dev) {
+        ok_ = hipGetDevice(&prev_) == hipSuccess;
+        if (ok_ && prev_ != dev) ok_ = hipSetDevice(dev) == hipSuccess;
+        changed_ = ok_ && prev_ != dev;
+    }
+    ~DeviceGuard() {
+        if (changed_) (void)hipSetDevice(prev_);
+    }
+    bool ok() const { return ok_; }
+
+  private:
+    int prev_ = 0;
+    bool ok_ = false, changed_ = false;
+};
+
+fftsplit_status_t check_plan(fftsplit_plan_t plan) {
+    if (!plan) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "plan is NULL");
+    if (plan->device < 0)
+        return fail(FFTSPLIT_ERROR_INVALID_VALUE, "plan was created for an architecture name only and cannot run");
+    return FFTSPLIT_SUCCESS;
+}
+
+fftsplit_status_t check_ptr(const void* p, const char* name) {
+    if (!p) return fail(FFTSPLIT_ERROR_INVALID_VALUE, std::string(name) + " is NULL");
+    if (!aligned16(p)) return fail(FFTSPLIT_ERROR_INVALID_VALUE, std::string(name) + " is not 16-byte aligned");
+    return FFTSPLIT_SUCCESS;
+}
+
+fftsplit_status_t check_workspace(fftsplit_plan_t plan, const void* ws, size_t bytes) {
+    if (fftsplit_status_t s = check_ptr(ws, "workspace")) return s;
+    if (bytes < plan->ws_bytes)
+        return fail(FFTSPLIT_ERROR_INSUFFICIENT_WORKSPACE,
+                    "workspace has " + std::to_string(bytes) + " bytes, plan needs " + std::to_string(plan->ws_bytes));
+    return FFTSPLIT_SUCCESS;
+}
+
+fftsplit_status_t check_bias(fftsplit_plan_t plan, const float* bias) {
+    if (plan->bias) return check_ptr(bias, "bias");
+    if (bias) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "bias given but the plan has no FFTSPLIT_BIAS flag");
+    return FFTSPLIT_SUCCESS;
+}
+
+fftsplit_status_t launched(hipError_t e, const char* what) {
+    if (e != hipSuccess) return fail(FFTSPLIT_ERROR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+    return FFTSPLIT_SUCCESS;
+}
+
+size_t x_bytes(fftsplit_plan_t p) { return size_t(p->prob.n) * p->prob.cin * p->prob.h * p->prob.w * 4; }
+size_t y_bytes(fftsplit_plan_t p) { return size_t(p->prob.n) * p->prob.cout * p->prob.h * p->prob.w * 4; }
+
+char* ws_at(void* ws, size_t off) { return static_cast<char*>(ws) + off; }
+
+}  // namespace
+
+FFTSPLIT_EXPORT fftsplit_status_t fftsplit_transform_weights(fftsplit_plan_t plan, const float* w, void* wspec,
+                                                             hipStream_t stream) {
+    set_error("");
+    if (fftsplit_status_t s = check_plan(plan)) return s;
+    if (fftsplit_status_t s = check_ptr(w, "w")) return s;
+    if (fftsplit_status_t s = check_ptr(wspec, "wspec")) return s;
+    const size_t wb = size_t(plan->prob.cout) * plan->prob.cin * plan->prob.k * plan->prob.k * 4;
+    if (overlap(w, wb, wspec, plan->wspec_bytes)) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "w overlaps wspec");
+    DeviceGuard g(plan->device);
+    if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
+    return launched(launch_weights(*plan, w, static_cast<float2*>(wspec), stream), "weight transform launch");
+}
+
+FFTSPLIT_EXPORT fftsplit_status_t fftsplit_forward(fftsplit_plan_t plan, const float* x, void* workspace,
+                                                   size_t workspace_bytes, hipStream_t stream) {
+    set_error("");
+    if (fftsplit_status_t s = check_plan(plan)) return s;
+    if (fftsplit_status_t s = check_ptr(x, "x")) return s;
+    if (fftsplit_status_t s = check_workspace(plan, workspace, workspace_bytes)) return s;
+    if (overlap(x, x_bytes(plan), workspace, plan->ws_bytes))
+        return fail(FFTSPLIT_ERROR_INVALID_VALUE, "x overlaps the workspace");
+    DeviceGuard g(plan->device);
+    if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
+    return launched(launch_forward(*plan, x, reinterpret_cast<float2*>(ws_at(workspace, plan->xspec_off)), stream),
+                    "forward patch transform launch");
+}
+
+FFTSPLIT_EXPORT fftsplit_status_t fftsplit_contract(fftsplit_plan_t plan, const void* wspec, void* workspace,
+                                                    size_t workspace_bytes, hipStream_t stream) {
+    set_error("");
+    if (fftsplit_status_t s = check_plan(plan)) return s;
+    if (fftsplit_status_t s = check_ptr(wspec, "wspec")) return s;
+    if (fftsplit_status_t s = check_workspace(plan, workspace, workspace_bytes)) return s;
+    if (overlap(wspec, plan->wspec_bytes, workspace, plan->ws_bytes))
+        return fail(FFTSPLIT_ERROR_INVALID_VALUE, "wspec overlaps the workspace");
+    DeviceGuard g(plan->device);
+    if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
+    return launched(launch_contract(*plan, reinterpret_cast<const float2*>(ws_at(workspace, plan->xspec_off)),
+                                    static_cast<const float2*>(wspec),
+                                    reinterpret_cast<float2*>(ws_at(workspace, plan->yspec_off)), stream),
+                    "contraction launch");
+}
+
+FFTSPLIT_EXPORT fftsplit_status_t fftsplit_inverse(fftsplit_plan_t plan, const float* bias, float* y,
+                                                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    set_error("");
+    if (fftsplit_status_t s = check_plan(plan)) return s;
+    if (fftsplit_status_t s = check_ptr(y, "y")) return s;
+    if (fftsplit_status_t s = check_bias(plan, bias)) return s;
+    if (fftsplit_status_t s = check_workspace(plan, workspace, workspace_bytes)) return s;
+    if (overlap(y, y_bytes(plan), workspace, plan->ws_bytes))
+        return fail(FFTSPLIT_ERROR_INVALID_VALUE, "y overlaps the workspace");
+    DeviceGuard g(plan->device);
+    if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
+    return launched(launch_inverse(*plan, reinterpret_cast<const float2*>(ws_at(workspace, plan->yspec_off)), bias, y,
+                                   plan->aux_bytes ? ws_at(workspace, plan->aux_off) : nullptr, stream),
+                    "inverse patch transform launch");
+}
+
+FFTSPLIT_EXPORT fftsplit_status_t fftsplit_conv2d(fftsplit_plan_t plan, const float* x, const void* wspec,
+                                                  const float* bias, float* y, void* workspace,
+                                                  size_t workspace_bytes, hipStream_t stream) {
+    set_error("");
+    if (fftsplit_status_t s = check_plan(plan)) return s;
+    if (fftsplit_status_t s = check_ptr(x, "x")) return s;
+    if (fftsplit_status_t s = check_ptr(wspec, "wspec")) return s;
+    if (fftsplit_status_t s = check_ptr(y, "y")) return s;
+    if (fftsplit_status_t s = check_bias(plan, bias)) return s;
+    if (fftsplit_status_t s = check_workspace(plan, workspace, workspace_bytes)) return s;
+    if (overlap(x, x_bytes(plan), y, y_bytes(plan))) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "y overlaps x");
+    if (overlap(x, x_bytes(plan), workspace, plan->ws_bytes) || overlap(y, y_bytes(plan), workspace, plan->ws_bytes) ||
+        overlap(wspec, plan->wspec_bytes, workspace, plan->ws_bytes) ||
+        overlap(wspec, plan->wspec_bytes, y, y_bytes(plan)))
+        return fail(FFTSPLIT_ERROR_INVALID_VALUE, "buffers overlap");
+    DeviceGuard g(plan->device);
+    if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
+    float2* xs = reinterpret_cast<float2*>(ws_at(workspace, plan->xspec_off));
+    float2* ys = reinterpret_cast<float2*>(ws_at(workspace, plan->yspec_off));
+    if (fftsplit_status_t s = launched(launch_forward(*plan, x, xs, stream), "forward patch transform launch")) return s;
+    if (fftsplit_status_t s = launched(launch_contract(*plan, xs, static_cast<const float2*>(wspec), ys, stream),
+                                       "contraction launch"))
+        return s;
+    return launched(launch_inverse(*plan, ys, bias, y, plan->aux_bytes ? ws_at(workspace, plan->aux_off) : nullptr,
+                                   stream),
+                    "inverse patch transform launch");
+}
+
+FFTSPLIT_EXPORT fftsplit_status_t fftsplit_maxpool2x2(const float* x, float* y, int n, int c, int h, int w,
+                                                      hipStream_t stream) {
+    set_error("");
+    if (n <= 0 || c <= 0 || h < 2 || w < 2) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "need n, c > 0 and h, w >= 2");
+    if (fftsplit_status_t s = check_ptr(x, "x")) return s;
+    if (fftsplit_status_t s = check_ptr(y, "y")) return s;
+    const size_t xb = size_t(n) * c * h * w * 4, yb = size_t(n) * c * (h / 2) * (w / 2) * 4;
+    if (overlap(x, xb, y, yb)) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "y overlaps x");
+    return launched(launch_maxpool(x, y, n, c, h, w, stream), "max-pool launch");
+}

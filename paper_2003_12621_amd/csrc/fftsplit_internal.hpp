@@ -1,0 +1,53 @@
+// Internal declarations shared by the host library and the kernel files.
+#pragma once
+
+#include <cstddef>
+#include <string>
+
+#include <hip/hip_runtime.h>
+
+#include "../../include/fftsplit.h"
+
+#define FFTSPLIT_EXPORT extern "C" __attribute__((visibility("default")))
+
+struct fftsplit_plan_s {
+    fftsplit_problem_t prob;
+    int device;                 // HIP ordinal, or -1 for an architecture-only plan
+    char arch[64];
+    int T, L, P;                // tile, FFT size, K/2
+    int th, tw, nt, ntp;        // tile grid, tiles, padded tiles
+    int bins, coutp;            // stored bins, padded output channels
+    bool oaa, bias, relu;
+    size_t wspec_bytes;
+    size_t xspec_off, xspec_bytes, yspec_off, yspec_bytes, aux_off, aux_bytes;
+    size_t ws_bytes;
+};
+
+namespace fftsplit {
+
+// Granularity of the contraction's output tiles (patches x channels).
+constexpr int kTileGranule = 64;
+constexpr int kCoutGranule = 64;
+
+// Number of stored frequency bins of an L x L real transform.
+__host__ __device__ constexpr int stored_bins(int L) { return L * L / 2 + 2; }
+
+// Bin index of (k1, k2) for k2 in [1, L/2-1]; and of the two real columns.
+__host__ __device__ constexpr int bin_mid(int L, int k1, int k2) { return (k2 - 1) * L + k1; }
+__host__ __device__ constexpr int bin_col0(int L, int k1) { return L * (L / 2 - 1) + k1; }
+__host__ __device__ constexpr int bin_colh(int L, int k1) { return L * (L / 2 - 1) + L / 2 + 1 + k1; }
+
+// Thread-local error detail for fftsplit_last_error().
+void set_error(const std::string& msg);
+fftsplit_status_t fail(fftsplit_status_t st, const std::string& msg);
+
+// Kernel launchers (one per .hip file); return hipSuccess or the launch error.
+hipError_t launch_weights(const fftsplit_plan_s& p, const float* w, float2* wspec, hipStream_t s);
+hipError_t launch_forward(const fftsplit_plan_s& p, const float* x, float2* xspec, hipStream_t s);
+hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xspec, const float2* wspec,
+                           float2* yspec, hipStream_t s);
+hipError_t launch_inverse(const fftsplit_plan_s& p, const float2* yspec, const float* bias, float* y,
+                          void* aux, hipStream_t s);
+hipError_t launch_maxpool(const float* x, float* y, int n, int c, int h, int w, hipStream_t s);
+
+}  // namespace fftsplit

@@ -1,0 +1,76 @@
+// Filter spectra, once per layer (Section 3.1, eq. 8 and the filter half of
+// eq. 9).
+//
+// Each K x K filter is zero-padded top-left to L x L and transformed.  The
+// padded filter has only K*K nonzeros, so each of its stored bins is a
+// direct K*K-term sum, evaluated in double precision with host-computed
+// double twiddles and rounded once to fp32.  A CNN layer is a
+// cross-correlation, so the stored value is the conjugate spectrum; the
+// inverse transform's 1/L^2 is folded in here so the hot path never scales.
+#include "fftsplit_internal.hpp"
+#include "fft_regs.hpp"
+
+namespace fftsplit {
+
+struct TwiddlesD {
+    double c[kTwN];
+    double s[kTwN];
+};
+
+__global__ __launch_bounds__(256) void weights_kernel(const float* __restrict__ w, float2* __restrict__ wspec,
+                                                      int cin, int cout, int coutp, int K, int L, int bins,
+                                                      TwiddlesD tw) {
+    const size_t total = size_t(bins) * cin * coutp;
+    const size_t idx = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (idx >= total) return;
+    const int co = int(idx % coutp);
+    const size_t rest = idx / coutp;
+    const int ci = int(rest % cin);
+    const int f = int(rest / cin);
+    if (co >= cout) {
+        wspec[idx] = make_float2(0.f, 0.f);
+        return;
+    }
+    // Decode the bin (k1, k2) from f (order documented in fftsplit.h).
+    const int h2 = L / 2;
+    int k1, k2;
+    if (f < L * (h2 - 1)) {
+        k2 = 1 + f / L;
+        k1 = f % L;
+    } else if (f < L * (h2 - 1) + h2 + 1) {
+        k2 = 0;
+        k1 = f - L * (h2 - 1);
+    } else {
+        k2 = h2;
+        k1 = f - L * (h2 - 1) - (h2 + 1);
+    }
+    const int step = kTwN / L;
+    const float* wp = w + (size_t(co) * cin + ci) * K * K;
+    double re = 0.0, im = 0.0;
+    for (int u = 0; u < K; ++u) {
+        for (int v = 0; v < K; ++v) {
+            const int e = ((u * k1 + v * k2) % L) * step;
+            const double val = double(wp[u * K + v]);
+            // conj(sum w exp(-2 pi i e / L)) = sum w exp(+2 pi i e / L)
+            re += val * tw.c[e];
+            im += val * tw.s[e];
+        }
+    }
+    const double inv = 1.0 / double(L * L);
+    wspec[idx] = make_float2(float(re * inv), float(im * inv));
+}
+
+hipError_t launch_weights(const fftsplit_plan_s& p, const float* w, float2* wspec, hipStream_t s) {
+    TwiddlesD tw;
+    for (int i = 0; i < kTwN; ++i) {
+        tw.c[i] = kTwCosD[i];
+        tw.s[i] = kTwSinD[i];
+    }
+    const size_t total = size_t(p.bins) * p.prob.cin * p.coutp;
+    const unsigned blocks = unsigned((total + 255) / 256);
+    hipLaunchKernelGGL(weights_kernel, dim3(blocks), dim3(256), 0, s, w, wspec, p.prob.cin, p.prob.cout, p.coutp,
+                       p.prob.k, p.L, p.bins, tw);
+    return hipGetLastError();
+}
+
+}  // namespace fftsplit

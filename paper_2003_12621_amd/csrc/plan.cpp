@@ -1,0 +1,246 @@
+// Plan creation: argument validation, tile-size choice and buffer sizes.
+//
+// The paper leaves the patch size free, to be picked from the hardware's
+// constraints (Section 3.1, first paragraph; Section 3.2).  Here the FFT
+// size L is restricted to the register transforms the kernels implement
+// (8, 16, 32), so T = L - K + 1, and a plan without an explicit tile picks
+// the L whose modelled time (streamed bytes at an effective bandwidth plus
+// contraction flops at an effective matrix-core rate) is smallest.
+#include <cerrno>
+#include <climits>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "fftsplit_internal.hpp"
+
+namespace fftsplit {
+
+static thread_local std::string g_last_error;
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+
+fftsplit_status_t fail(fftsplit_status_t st, const std::string& msg) {
+    g_last_error = msg;
+    return st;
+}
+
+static size_t round_up(size_t v, size_t g) { return (v + g - 1) / g * g; }
+
+// Multiply with overflow detection.
+static bool mul_ok(size_t a, size_t b, size_t* out) {
+    if (a != 0 && b > SIZE_MAX / a) return false;
+    *out = a * b;
+    return true;
+}
+
+// Effective rates of the cost model (bytes/s and flop/s) -- deliberately
+// conservative fractions of the 8 TB/s HBM and 157 TFLOP/s fp32 matrix peaks.
+static constexpr double kModelBandwidth = 5.0e12;
+static constexpr double kModelMatrixRate = 100.0e12;
+
+struct Geometry {
+    int T, L, th, tw, nt, ntp, bins, coutp;
+    double model_seconds;
+};
+
+static Geometry geometry(const fftsplit_problem_t& p, int L) {
+    Geometry g{};
+    g.L = L;
+    g.T = L - p.k + 1;
+    g.th = (p.h + g.T - 1) / g.T;
+    g.tw = (p.w + g.T - 1) / g.T;
+    const double nt = double(p.n) * g.th * g.tw;
+    g.nt = nt > INT_MAX ? -1 : int(nt);
+    g.ntp = g.nt < 0 ? -1 : int(round_up(size_t(g.nt), kTileGranule));
+    g.bins = stored_bins(L);
+    g.coutp = int(round_up(size_t(p.cout), kCoutGranule));
+    const double F = g.bins, ntp = double(g.ntp), cin = p.cin, coutp = g.coutp;
+    const double img = double(p.n) * p.h * p.w;
+    const double fwd = 4.0 * img * cin + 8.0 * F * cin * ntp;
+    const double con_b = 8.0 * F * (cin * ntp + cin * coutp + coutp * ntp);
+    const double con_f = 8.0 * F * cin * coutp * ntp;
+    const double inv = 8.0 * F * coutp * ntp + 4.0 * img * p.cout;
+    const double con = con_f / kModelMatrixRate > con_b / kModelBandwidth ? con_f / kModelMatrixRate
+                                                                          : con_b / kModelBandwidth;
+    g.model_seconds = fwd / kModelBandwidth + con + inv / kModelBandwidth;
+    return g;
+}
+
+static bool supported_L(int L) { return L == 8 || L == 16 || L == 32; }
+
+static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, const char* arch,
+                                    fftsplit_plan_t* out) {
+    if (!prob || !out) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "problem and output pointers must be non-NULL");
+    const fftsplit_problem_t p = *prob;
+    if (p.n <= 0 || p.cin <= 0 || p.h <= 0 || p.w <= 0 || p.cout <= 0 || p.k <= 0)
+        return fail(FFTSPLIT_ERROR_INVALID_VALUE, "all dimensions must be positive");
+    if (p.tile < 0) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "tile must be >= 0 (0 = choose)");
+    const unsigned known = FFTSPLIT_OVERLAP_ADD | FFTSPLIT_BIAS | FFTSPLIT_RELU;
+    if (p.flags & ~known) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "unknown flag bits");
+    if (p.k % 2 == 0) return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "kernel size must be odd");
+    if (p.stride != 1) return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "only stride 1 is supported");
+    if (p.pad != p.k / 2) return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "only 'same' padding (pad = k/2) is supported");
+    if (p.k > 31) return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "kernel larger than the largest FFT size");
+    if (p.cin > 65535 || p.cout > 65535)
+        return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "channel counts above 65535 are not supported");
+    const bool oaa = (p.flags & FFTSPLIT_OVERLAP_ADD) != 0;
+
+    int tile = p.tile;
+    if (tile == 0) {
+        const char* env = std::getenv("FFTSPLIT_TILE");
+        if (env && *env) {
+            char* end = nullptr;
+            errno = 0;
+            long v = std::strtol(env, &end, 10);
+            if (errno || !end || *end || v <= 0 || v > 32)
+                return fail(FFTSPLIT_ERROR_INVALID_VALUE, "FFTSPLIT_TILE must be a positive integer <= 32");
+            tile = int(v);
+        }
+    }
+    Geometry g{};
+    if (tile > 0) {
+        const int L = tile + p.k - 1;
+        if (!supported_L(L))
+            return fail(FFTSPLIT_ERROR_NOT_SUPPORTED,
+                        "tile + k - 1 must be 8, 16 or 32 (got " + std::to_string(L) + ")");
+        g = geometry(p, L);
+    } else {
+        bool have = false;
+        for (int L : {8, 16, 32}) {
+            const int T = L - p.k + 1;
+            if (T < 1 || (oaa && T < p.k - 1)) continue;
+            Geometry c = geometry(p, L);
+            if (c.nt < 0) continue;
+            if (!have || c.model_seconds < g.model_seconds) { g = c; have = true; }
+        }
+        if (!have) return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "no FFT size in {8,16,32} fits this kernel");
+    }
+    if (oaa && g.T < p.k - 1)
+        return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "overlap-add needs tile >= k - 1");
+    if (g.nt < 0 || g.ntp < 0 || g.ntp / kTileGranule > INT_MAX / 2)
+        return fail(FFTSPLIT_ERROR_INVALID_VALUE, "too many patches");
+
+    // Byte sizes with overflow checks.
+    size_t xs, ys, wsb, tmp;
+    if (!mul_ok(size_t(g.bins) * 8, size_t(p.cin), &tmp) || !mul_ok(tmp, size_t(g.ntp), &xs) ||
+        !mul_ok(size_t(g.bins) * 8, size_t(g.coutp), &tmp) || !mul_ok(tmp, size_t(g.ntp), &ys) ||
+        !mul_ok(size_t(g.bins) * 8, size_t(p.cin), &tmp) || !mul_ok(tmp, size_t(g.coutp), &wsb))
+        return fail(FFTSPLIT_ERROR_INVALID_VALUE, "buffer sizes overflow size_t");
+    size_t img_elems;
+    if (!mul_ok(size_t(p.n) * size_t(p.h), size_t(p.w), &tmp) ||
+        !mul_ok(tmp, size_t(p.cin > p.cout ? p.cin : p.cout), &img_elems))
+        return fail(FFTSPLIT_ERROR_INVALID_VALUE, "tensor sizes overflow size_t");
+
+    // Architecture check.
+    char archbuf[64] = {0};
+    if (device >= 0) {
+        hipDeviceProp_t prop;
+        hipError_t e = hipGetDeviceProperties(&prop, device);
+        if (e != hipSuccess)
+            return fail(FFTSPLIT_ERROR_DEVICE, std::string("hipGetDeviceProperties: ") + hipGetErrorString(e));
+        std::snprintf(archbuf, sizeof(archbuf), "%s", prop.gcnArchName);
+    } else {
+        std::snprintf(archbuf, sizeof(archbuf), "%s", arch ? arch : "");
+    }
+    if (std::strncmp(archbuf, "gfx950", 6) != 0)
+        return fail(FFTSPLIT_ERROR_ARCH, std::string("device architecture '") + archbuf + "' is not gfx950");
+
+    fftsplit_plan_s* plan = new (std::nothrow) fftsplit_plan_s();
+    if (!plan) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "out of host memory");
+    plan->prob = p;
+    plan->prob.tile = g.T;
+    plan->device = device;
+    std::snprintf(plan->arch, sizeof(plan->arch), "%s", archbuf);
+    plan->T = g.T;
+    plan->L = g.L;
+    plan->P = p.k / 2;
+    plan->th = g.th;
+    plan->tw = g.tw;
+    plan->nt = g.nt;
+    plan->ntp = g.ntp;
+    plan->bins = g.bins;
+    plan->coutp = g.coutp;
+    plan->oaa = oaa;
+    plan->bias = (p.flags & FFTSPLIT_BIAS) != 0;
+    plan->relu = (p.flags & FFTSPLIT_RELU) != 0;
+    plan->wspec_bytes = wsb;
+    plan->xspec_off = 0;
+    plan->xspec_bytes = xs;
+    plan->yspec_off = round_up(xs, 256);
+    plan->yspec_bytes = ys;
+    plan->aux_off = round_up(plan->yspec_off + ys, 256);
+    plan->aux_bytes = 0;
+    plan->ws_bytes = plan->aux_off + plan->aux_bytes;
+
+    const char* log = std::getenv("FFTSPLIT_LOG");
+    if (log && *log && *log != '0') {
+        std::fprintf(stderr,
+                     "[fftsplit] plan n=%d cin=%d %dx%d cout=%d k=%d -> T=%d L=%d tiles=%d(%d) bins=%d %s "
+                     "model=%.1f us wspec=%zu ws=%zu\n",
+                     p.n, p.cin, p.h, p.w, p.cout, p.k, g.T, g.L, g.nt, g.ntp, g.bins, oaa ? "oaa" : "os",
+                     g.model_seconds * 1e6, wsb, plan->ws_bytes);
+    }
+    *out = plan;
+    return FFTSPLIT_SUCCESS;
+}
+
+}  // namespace fftsplit
+
+using namespace fftsplit;
+
+FFTSPLIT_EXPORT fftsplit_status_t fftsplit_plan(const fftsplit_problem_t* prob, int device, fftsplit_plan_t* out) {
+    set_error("");
+    if (device < 0) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "device ordinal must be >= 0");
+    return build_plan(prob, device, nullptr, out);
+}
+
+FFTSPLIT_EXPORT fftsplit_status_t fftsplit_plan_for_arch(const fftsplit_problem_t* prob, const char* arch,
+                                                         fftsplit_plan_t* out) {
+    set_error("");
+    if (!arch) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "architecture string must be non-NULL");
+    return build_plan(prob, -1, arch, out);
+}
+
+FFTSPLIT_EXPORT fftsplit_status_t fftsplit_plan_info(fftsplit_plan_t plan, fftsplit_plan_info_t* out) {
+    set_error("");
+    if (!plan || !out) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "plan and output must be non-NULL");
+    fftsplit_plan_info_t i{};
+    i.tile = plan->T;
+    i.nfft = plan->L;
+    i.tiles_h = plan->th;
+    i.tiles_w = plan->tw;
+    i.tiles = plan->nt;
+    i.tiles_padded = plan->ntp;
+    i.bins = plan->bins;
+    i.cout_padded = plan->coutp;
+    i.flags = plan->prob.flags;
+    i.wspec_bytes = plan->wspec_bytes;
+    i.workspace_bytes = plan->ws_bytes;
+    i.xspec_offset = plan->xspec_off;
+    i.xspec_bytes = plan->xspec_bytes;
+    i.yspec_offset = plan->yspec_off;
+    i.yspec_bytes = plan->yspec_bytes;
+    i.aux_offset = plan->aux_off;
+    i.aux_bytes = plan->aux_bytes;
+    *out = i;
+    return FFTSPLIT_SUCCESS;
+}
+
+FFTSPLIT_EXPORT void fftsplit_plan_destroy(fftsplit_plan_t plan) { delete plan; }
+
+FFTSPLIT_EXPORT const char* fftsplit_status_string(fftsplit_status_t st) {
+    switch (st) {
+        case FFTSPLIT_SUCCESS: return "success";
+        case FFTSPLIT_ERROR_INVALID_VALUE: return "invalid value";
+        case FFTSPLIT_ERROR_NOT_SUPPORTED: return "not supported";
+        case FFTSPLIT_ERROR_INSUFFICIENT_WORKSPACE: return "insufficient workspace";
+        case FFTSPLIT_ERROR_DEVICE: return "device error";
+        case FFTSPLIT_ERROR_ARCH: return "unsupported architecture";
+    }
+    return "unknown status";
+}
+
+FFTSPLIT_EXPORT const char* fftsplit_last_error(void) { return g_last_error.c_str(); }

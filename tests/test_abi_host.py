@@ -1,0 +1,167 @@
+"""Host-side checks of the C ABI: the library loads, exports what the header
+declares, and plans validate arguments and report the documented geometry.
+No kernel is launched (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2003_12621_amd as fs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fftsplit.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fftsplit_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert len(names) >= 12
+    handle = ctypes.CDLL(fs.LIB_PATH)
+    for name in names:
+        assert hasattr(handle, name), name
+    # and the binding knows a signature for each of them
+    assert set(names) == set(fs._SIGNATURES)
+
+
+def plan(**kw):
+    base = dict(n=1, cin=3, h=32, w=32, cout=16, k=3, tile=6)
+    base.update(kw)
+    return fs.Plan(arch="gfx950:sramecc+:xnack-", **base)
+
+
+def status_of(**kw):
+    try:
+        plan(**kw)
+    except fs.FftsplitError as e:
+        return e.status
+    return fs.SUCCESS
+
+
+def test_first_config_geometry():
+    p = plan()
+    i = p.info
+    assert (i.tile, i.nfft, i.tiles_h, i.tiles_w, i.tiles) == (6, 8, 6, 6, 36)
+    assert i.bins == 8 * 8 // 2 + 2
+    assert i.tiles_padded % 64 == 0 and i.tiles_padded >= 36
+    assert i.cout_padded >= 16
+    assert i.wspec_bytes == 8 * i.bins * 3 * i.cout_padded
+    assert i.xspec_bytes == 8 * i.bins * 3 * i.tiles_padded
+    assert i.yspec_bytes == 8 * i.bins * i.cout_padded * i.tiles_padded
+    assert i.yspec_offset >= i.xspec_offset + i.xspec_bytes
+    assert i.workspace_bytes >= i.yspec_offset + i.yspec_bytes
+
+
+@pytest.mark.parametrize("h,w,t,k", [(56, 56, 28, 5), (56, 56, 12, 5), (224, 224, 30, 3), (224, 224, 6, 3),
+                                     (112, 112, 14, 3), (7, 9, 6, 3), (5, 5, 8, 1)])
+def test_tile_grid_and_fft_size(h, w, t, k):
+    p = plan(n=2, cin=4, h=h, w=w, cout=8, k=k, tile=t)
+    assert p.info.nfft == t + k - 1
+    assert p.info.tiles_h == -(-h // t) and p.info.tiles_w == -(-w // t)
+    assert p.info.tiles == 2 * p.info.tiles_h * p.info.tiles_w
+
+
+def test_status_codes():
+    assert status_of() == fs.SUCCESS
+    assert status_of(k=4, tile=5) == fs.ERROR_NOT_SUPPORTED          # even kernel
+    assert status_of(tile=7) == fs.ERROR_NOT_SUPPORTED               # L = 9
+    assert status_of(n=0) == fs.ERROR_INVALID_VALUE
+    assert status_of(cin=-1) == fs.ERROR_INVALID_VALUE
+    assert status_of(tile=-2) == fs.ERROR_INVALID_VALUE
+    assert status_of(stride=2) == fs.ERROR_NOT_SUPPORTED
+    assert status_of(pad=0) == fs.ERROR_NOT_SUPPORTED
+    assert status_of(k=33, tile=0) == fs.ERROR_NOT_SUPPORTED
+    assert status_of(k=5, tile=4, mode="oaa") == fs.SUCCESS          # T = K - 1
+    assert status_of(k=7, tile=2, mode="oaa") == fs.ERROR_NOT_SUPPORTED  # T < K - 1
+    assert status_of(cin=70000, tile=6) == fs.ERROR_NOT_SUPPORTED
+
+
+def test_wrong_architecture_is_rejected():
+    with pytest.raises(fs.FftsplitError) as e:
+        fs.Plan(n=1, cin=3, h=32, w=32, cout=16, k=3, tile=6, arch="gfx942:sramecc+:xnack-")
+    assert e.value.status == fs.ERROR_ARCH
+    assert "gfx942" in str(e.value)
+
+
+def test_status_strings_and_last_error():
+    for code in range(6):
+        assert fs.status_string(code)
+    assert fs.status_string(99) == "unknown status"
+    status_of(tile=7)
+    assert "8, 16 or 32" in fs.last_error()
+    plan()
+    assert fs.last_error() == ""
+
+
+def test_unknown_flags_rejected():
+    prob = fs.problem(1, 3, 32, 32, 16, 3, 6)
+    prob.flags = 64
+    h = ctypes.c_void_p()
+    st = fs.lib().fftsplit_plan_for_arch(ctypes.byref(prob), b"gfx950", ctypes.byref(h))
+    assert st == fs.ERROR_INVALID_VALUE
+
+
+def test_null_arguments():
+    h = ctypes.c_void_p()
+    L = fs.lib()
+    assert L.fftsplit_plan_for_arch(None, b"gfx950", ctypes.byref(h)) == fs.ERROR_INVALID_VALUE
+    prob = fs.problem(1, 3, 32, 32, 16, 3, 6)
+    assert L.fftsplit_plan_for_arch(ctypes.byref(prob), None, ctypes.byref(h)) == fs.ERROR_INVALID_VALUE
+    assert L.fftsplit_plan_info(None, ctypes.byref(fs.PlanInfo())) == fs.ERROR_INVALID_VALUE
+    L.fftsplit_plan_destroy(None)
+
+
+def test_arch_only_plan_cannot_launch():
+    p = plan()
+    L = fs.lib()
+    fake = ctypes.c_void_p(1 << 20)
+    st = L.fftsplit_conv2d(p._h, fake, fake, None, fake, fake, 1 << 30, None)
+    assert st == fs.ERROR_INVALID_VALUE
+    assert "architecture name only" in fs.last_error()
+    assert L.fftsplit_forward(p._h, fake, fake, 1 << 30, None) == fs.ERROR_INVALID_VALUE
+
+
+def test_auto_tile_choice_and_env_override(monkeypatch):
+    monkeypatch.delenv("FFTSPLIT_TILE", raising=False)
+    p = plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=0)
+    assert p.info.nfft in (8, 16, 32) and p.info.tile == p.info.nfft - 4
+    monkeypatch.setenv("FFTSPLIT_TILE", "12")
+    p = plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=0)
+    assert p.info.tile == 12
+    # an explicit tile wins over the environment
+    p = plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28)
+    assert p.info.tile == 28
+    monkeypatch.setenv("FFTSPLIT_TILE", "abc")
+    assert status_of(tile=0) == fs.ERROR_INVALID_VALUE
+
+
+def test_bin_order_matches_header():
+    for L in (8, 16, 32):
+        coords = fs.bin_coords(L)
+        assert len(coords) == L * L // 2 + 2
+        assert len(set(coords)) == len(coords)
+        # every (k1, k2) with k2 in [0, L/2] is stored or is the conjugate of a stored bin
+        stored = set(coords)
+        for k1 in range(L):
+            for k2 in range(L // 2 + 1):
+                mirror = ((-k1) % L, (-k2) % L)
+                assert (k1, k2) in stored or mirror in stored
+
+
+def test_spectra_layout_helpers_roundtrip():
+    import numpy as np
+    from spectra_layout import full_to_stored, stored_to_full, rel_l2
+    rng = np.random.default_rng(3)
+    for L in (8, 16, 32):
+        a = rng.standard_normal((2, 3, L, L))
+        full = np.fft.fft2(a)
+        st = full_to_stored(full)
+        assert st.shape == (L * L // 2 + 2, 2, 3)
+        np.testing.assert_allclose(stored_to_full(st, L), full, rtol=0, atol=1e-12)
+    # the error measure sees imaginary parts
+    assert rel_l2(np.array([1 + 1j]), np.array([1 + 0j])) == 1.0

@@ -1,0 +1,133 @@
+"""Stage-by-stage parity of the HIP kernels against the oracle's steps.
+
+Each kernel is fed inputs the oracle also sees and compared element by
+element, so a failure names the stage:
+  weights  -- eq. 8: conj(DFT(zero-padded filter)) / L^2 at the stored bins
+  forward  -- eqs. 4-6 + forward DFT of every padded patch
+  contract -- eq. 9 summed over input channels, on the GPU's own spectra
+  inverse  -- eq. 10 (inverse DFT, crop/concatenate), bias, ReLU, on the
+              GPU's own output spectra
+Tolerances: spectra evaluated in double and rounded once (weights) must be
+within 1e-6 relative; fp32 transforms and sums within 2e-6 relative L2.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from workloads import make_config, small_layer, make_random_bias
+
+from spectra_layout import full_to_stored, stored_to_full, rel_l2, rel_max
+
+torch = pytest.importorskip("torch")
+fs = pytest.importorskip("paper_2003_12621_amd")
+
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    # name, (n, cin, h, w, cout, k), tile, mode
+    ("c1_L8", (1, 3, 32, 32, 16, 3), 6),
+    ("ragged_L16_k5", (2, 5, 19, 23, 10, 5), 12),
+    ("ragged_L32", (3, 4, 37, 30, 7, 3), 30),
+    ("k1_L8", (1, 2, 17, 9, 3, 1), 8),
+    ("k7_L16", (1, 3, 21, 20, 5, 7), 10),
+]
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _setup(shape, tile, mode="os", seed=5):
+    n, cin, h, w, cout, k = shape
+    x, wt = small_layer(n, cin, h, w, cout, k, seed=seed)
+    plan = fs.Plan(n, cin, h, w, cout, k, tile=tile, mode=mode)
+    return x, wt, plan
+
+
+@pytest.mark.parametrize("name,shape,tile", CASES)
+def test_weight_spectra(name, shape, tile):
+    x, wt, plan = _setup(shape, tile)
+    L = plan.nfft
+    wspec = plan.transform_weights(_dev(wt))
+    torch.cuda.synchronize()
+    got = plan.wspec_view(wspec).cpu().numpy()                     # [bins, cin, coutp]
+    ref = full_to_stored(np.conj(oracle.filter_spectra(wt, L)) / (L * L))   # [bins, cout, cin]
+    ref = ref.transpose(0, 2, 1)
+    cout = shape[4]
+    assert rel_max(got[:, :, :cout], ref) < 1e-6
+    assert np.all(got[:, :, cout:] == 0)
+
+
+@pytest.mark.parametrize("mode", ["os", "oaa"])
+@pytest.mark.parametrize("name,shape,tile", CASES)
+def test_forward_spectra(name, shape, tile, mode):
+    n, cin, h, w, cout, k = shape
+    if mode == "oaa" and tile < k - 1:
+        pytest.skip("overlap-add needs T >= K - 1")
+    x, wt, plan = _setup(shape, tile, mode)
+    ws = plan.new_workspace()
+    plan.forward(_dev(x), ws)
+    torch.cuda.synchronize()
+    got = plan.xspec_view(ws).cpu().numpy()                        # [bins, cin, ntp]
+    ref = oracle.patch_spectra(x, tile, k, mode)                   # [n, th, tw, cin, L, L]
+    nt = plan.info.tiles
+    ref = full_to_stored(ref.reshape(nt, cin, plan.nfft, plan.nfft))  # [bins, nt, cin]
+    ref = ref.transpose(0, 2, 1)
+    assert rel_l2(got[:, :, :nt], ref) < 2e-6
+    assert rel_max(got[:, :, :nt], ref) < 1e-5
+    assert np.all(got[:, :, nt:] == 0), "padding patches must have zero spectra"
+
+
+@pytest.mark.parametrize("name,shape,tile", CASES)
+def test_contraction(name, shape, tile):
+    n, cin, h, w, cout, k = shape
+    x, wt, plan = _setup(shape, tile)
+    ws = plan.new_workspace()
+    wspec = plan.transform_weights(_dev(wt))
+    plan.forward(_dev(x), ws)
+    plan.contract(wspec, ws)
+    torch.cuda.synchronize()
+    X = plan.xspec_view(ws).cpu().numpy().astype(np.complex128)     # [bins, cin, ntp]
+    W = plan.wspec_view(wspec).cpu().numpy().astype(np.complex128)  # [bins, cin, coutp]
+    Y = plan.yspec_view(ws).cpu().numpy()                           # [bins, coutp, ntp]
+    # oracle step 4 with xs [t, ci, bins] and ws [co, ci, bins]; the stored
+    # filter spectra are already conjugated, so they enter as conj(W).
+    ref = oracle.hadamard_channel_sum(X.transpose(2, 1, 0), np.conj(W).transpose(2, 1, 0))  # [t, co, bins]
+    ref = ref.transpose(2, 1, 0)                                    # [bins, co, t]
+    assert rel_l2(Y, ref) < 2e-6
+    assert rel_max(Y, ref) < 1e-5
+
+
+@pytest.mark.parametrize("relu", [False, True])
+@pytest.mark.parametrize("name,shape,tile", CASES)
+def test_inverse_placement(name, shape, tile, relu):
+    n, cin, h, w, cout, k = shape
+    x, wt = small_layer(n, cin, h, w, cout, k, seed=6)
+    plan = fs.Plan(n, cin, h, w, cout, k, tile=tile, bias=True, relu=relu)
+    L = plan.nfft
+    b = make_random_bias(cout, cin, k, seed=7)
+    ws = plan.new_workspace()
+    wspec = plan.transform_weights(_dev(wt))
+    plan.forward(_dev(x), ws)
+    plan.contract(wspec, ws)
+    y = plan.inverse(ws, bias=_dev(b))
+    torch.cuda.synchronize()
+    Y = plan.yspec_view(ws).cpu().numpy()                            # [bins, coutp, ntp]
+    nt = plan.info.tiles
+    th, tw = plan.info.tiles_h, plan.info.tiles_w
+    full = stored_to_full(Y[:, :cout, :nt], L)                       # [cout, nt, L, L]
+    full = full.transpose(1, 0, 2, 3).reshape(n, th, tw, cout, L, L)
+    # The stored output spectra carry the 1/L^2 of the inverse already; the
+    # oracle's inverse divides by L^2 itself.
+    ref = oracle.inverse_place(full * (L * L), h, w, tile, k, "os", b, relu)
+    got = y.cpu().numpy()
+    assert rel_l2(got, ref) < 2e-6
+    assert rel_max(got, ref) < 1e-5
+
+
+def test_maxpool_exact():
+    rng = np.random.default_rng(8)
+    for shape in [(2, 3, 8, 8), (1, 5, 7, 9), (4, 64, 224, 224), (1, 1, 2, 2)]:
+        x = rng.standard_normal(shape).astype(np.float32)
+        got = fs.maxpool2x2(_dev(x)).cpu().numpy()
+        np.testing.assert_array_equal(got, oracle.maxpool2x2(x))
