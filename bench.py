@@ -107,6 +107,8 @@ def main():
     ap.add_argument("--mode", default="os", choices=["os", "oaa"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true")
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="before timing, copy a buffer of this many MiB 3 times (calibrates HBM counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -134,6 +136,14 @@ def main():
     wspec = plan.transform_weights(wd)
     ws = plan.new_workspace()
     y = plan.new_output()
+    if args.copy_probe_mb > 0:
+        nbytes = args.copy_probe_mb << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     torch.cuda.synchronize()
 
     def step(evs=None):

@@ -1,115 +1,173 @@
 // Inverse patch transform with placement, bias and ReLU (Section 3.1,
 // eq. 10 and the concatenation that follows it).
 //
-// A workgroup owns TG consecutive patches of one output channel; L/2
-// threads per (patch, channel):
-//   1. column pass: thread j >= 1 inverse-transforms column k2 = j; thread 0
-//      rebuilds the full Hermitian columns k2 = 0 and k2 = L/2 from their
-//      stored halves, packs them as one complex sequence and inverse-
-//      transforms it (both results are real);
+// A workgroup owns TG consecutive patches of one output channel, with L/2
+// threads per patch:
+//   1. column pass (patch index fastest across lanes, so each bin of the TG
+//      patches is one contiguous 8*TG-byte read): thread j >= 1 inverse-
+//      transforms column k2 = j; thread 0 rebuilds the Hermitian columns
+//      k2 = 0 and k2 = L/2 from their stored halves, packs them as one
+//      complex sequence and inverse-transforms it (both results are real);
 //   2. row pass through LDS: thread j rebuilds rows 2j and 2j+1 over all L
-//      bins from Hermitian symmetry, packs them as one complex sequence
-//      (row 2j real, row 2j+1 imaginary) and inverse-transforms it;
-//   3. overlap-save: the top-left T x T block is the output tile (crop), it
-//      is written at the tile's place (concatenation) with bias and ReLU.
-// The 1/L^2 of the inverse is already in the filter spectra.
+//      bins from Hermitian symmetry, packs them as one complex sequence (row
+//      2j real, row 2j+1 imaginary) and inverse-transforms it;
+//   3. overlap-save placement: the top-left T x T block of each patch is its
+//      output tile (the crop), staged in LDS and written back row by row
+//      with bias and ReLU; horizontally adjacent patches of a group land in
+//      one contiguous run of the output row (the concatenation).
+// The inverse's 1/L^2 is already folded into the filter spectra.
 #include "fftsplit_internal.hpp"
 #include "fft_regs.hpp"
+#include "launch_util.hpp"
 
 namespace fftsplit {
+
+template <int L, int TG>
+struct InvShape {
+    static constexpr int H2 = L / 2;
+    static constexpr int NT = TG * H2;
+    static constexpr int TP = H2 + 1;             // half-spectrum row pitch (float2)
+    static constexpr int TTS = L * TP + 2;        // half-spectrum patch stride (float2)
+    static constexpr int SP = L + 1;              // staged tile row pitch (floats)
+    static constexpr int STS = L * SP + 1;        // staged tile patch stride (floats)
+    // store phase: lanes = q (L) x u_sub (US) x m_sub (MS)
+    static constexpr int US = (L == 32) ? 1 : (L == 16 ? 4 : 8);
+    static constexpr int MS = NT / (L * US);
+    static constexpr int TB_BYTES = TG * TTS * 8;
+    static constexpr int ST_BYTES = TG * STS * 4;
+    static constexpr int LDS_BYTES = TB_BYTES > ST_BYTES ? TB_BYTES : ST_BYTES;
+    static_assert(NT % (L * US) == 0 && TG % US == 0 && L % MS == 0, "store-phase lane split");
+};
 
 template <int L, int TG>
 __global__ __launch_bounds__(TG * (L / 2)) void inverse_os_kernel(const float2* __restrict__ ys,
                                                                   const float* __restrict__ bias,
                                                                   float* __restrict__ y, int cout, int coutp, int h,
                                                                   int w, int T, int th, int tw, int nt, int ntp,
-                                                                  int relu) {
-    constexpr int H2 = L / 2;
-    constexpr int TP = H2 + 1;
-    __shared__ float2 tb[TG * L * TP];
+                                                                  int ngroups, int relu) {
+    using S = InvShape<L, TG>;
+    constexpr int H2 = S::H2, NT = S::NT, TP = S::TP, TTS = S::TTS, SP = S::SP, STS = S::STS;
+    extern __shared__ float4 lds_raw[];
+    float2* tb = reinterpret_cast<float2*>(lds_raw);
+    float* st = reinterpret_cast<float*>(lds_raw);
+    __shared__ float* dst_base[TG];
+    __shared__ int rows_ok[TG], cols_ok[TG];
 
     const int tid = threadIdx.x;
-    const int co = blockIdx.y;
-    const int t0 = blockIdx.x * TG;
-    const int u = tid % TG;
-    const int j = tid / TG;
+    const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
+    const int g = lb % ngroups;
+    const int co = lb / ngroups;
+    const int t0 = g * TG;
 
-    const size_t bs = size_t(coutp) * ntp;
-    const float2* in = ys + size_t(co) * ntp + t0 + u;
+    if (tid < TG) {
+        const int t = t0 + tid;
+        int ro = 0, cw = 0;
+        float* d = y;
+        if (t < nt) {
+            const int b = t % tw;
+            const int rest = t / tw;
+            const int a = rest % th;
+            const int img = rest / th;
+            ro = min(T, h - a * T);
+            cw = min(T, w - b * T);
+            d = y + ((size_t(img) * cout + co) * h + size_t(a) * T) * size_t(w) + size_t(b) * T;
+        }
+        dst_base[tid] = d;
+        rows_ok[tid] = ro;
+        cols_ok[tid] = cw;
+    }
 
     // 1. column pass
-    float2 cz[L];
-    if (j == 0) {
-        float2 y0[H2 + 1], yh[H2 + 1];
+    {
+        const int u = tid % TG;
+        const int j = tid / TG;
+        const size_t bs = size_t(coutp) * ntp;
+        const float2* in = ys + size_t(co) * ntp + t0 + u;
+        float2 cz[L];
+        if (j == 0) {
+            float2 y0[H2 + 1], yh[H2 + 1];
 #pragma unroll
-        for (int k1 = 0; k1 <= H2; ++k1) {
-            y0[k1] = in[size_t(bin_col0(L, k1)) * bs];
-            yh[k1] = in[size_t(bin_colh(L, k1)) * bs];
-        }
-#pragma unroll
-        for (int k1 = 0; k1 < L; ++k1) {
-            if (k1 <= H2) {  // U = Y0 + i YH
-                cz[k1] = make_float2(y0[k1].x - yh[k1].y, y0[k1].y + yh[k1].x);
-            } else {         // Y0[k1] = conj(Y0[L-k1]), likewise YH
-                const float2 a = y0[L - k1], b = yh[L - k1];
-                cz[k1] = make_float2(a.x + b.y, b.x - a.y);
+            for (int k1 = 0; k1 <= H2; ++k1) {
+                y0[k1] = in[size_t(bin_col0(L, k1)) * bs];
+                yh[k1] = in[size_t(bin_colh(L, k1)) * bs];
             }
+#pragma unroll
+            for (int k1 = 0; k1 < L; ++k1) {
+                if (k1 <= H2) {  // U = Y0 + i YH
+                    cz[k1] = make_float2(y0[k1].x - yh[k1].y, y0[k1].y + yh[k1].x);
+                } else {         // Y0[k1] = conj(Y0[L-k1]), likewise YH
+                    const float2 a = y0[L - k1], b = yh[L - k1];
+                    cz[k1] = make_float2(a.x + b.y, b.x - a.y);
+                }
+            }
+        } else {
+            const float2* src = in + size_t(bin_mid(L, 0, j)) * bs;
+#pragma unroll
+            for (int k1 = 0; k1 < L; ++k1) cz[k1] = src[size_t(k1) * bs];
         }
-    } else {
-        const float2* src = in + size_t(bin_mid(L, 0, j)) * bs;
+        fft<L, true>(cz);
+        float2* cb = tb + u * TTS;
+        if (j == 0) {
 #pragma unroll
-        for (int k1 = 0; k1 < L; ++k1) cz[k1] = src[size_t(k1) * bs];
-    }
-    fft<L, true>(cz);
-    if (j == 0) {
+            for (int m = 0; m < L; ++m) {
+                cb[m * TP] = make_float2(cz[m].x, 0.f);
+                cb[m * TP + H2] = make_float2(cz[m].y, 0.f);
+            }
+        } else {
 #pragma unroll
-        for (int m = 0; m < L; ++m) {
-            tb[(u * L + m) * TP] = make_float2(cz[m].x, 0.f);
-            tb[(u * L + m) * TP + H2] = make_float2(cz[m].y, 0.f);
+            for (int m = 0; m < L; ++m) cb[m * TP + j] = cz[m];
         }
-    } else {
-#pragma unroll
-        for (int m = 0; m < L; ++m) tb[(u * L + m) * TP + j] = cz[m];
     }
     __syncthreads();
 
-    // 2. row pass for rows 2j, 2j+1
-    float2 z[L];
-    const float2* ra = tb + (u * L + 2 * j) * TP;
-    const float2* rb = ra + TP;
+    // 2. row pass (j fastest across lanes)
+    {
+        const int j = tid % H2;
+        const int u = tid / H2;
+        float2 z[L];
+        const float2* ra = tb + u * TTS + 2 * j * TP;
+        const float2* rb = ra + TP;
 #pragma unroll
-    for (int k2 = 0; k2 < L; ++k2) {
-        if (k2 <= H2) {
-            const float2 a = ra[k2], b = rb[k2];
-            z[k2] = make_float2(a.x - b.y, a.y + b.x);
-        } else {
-            const float2 a = ra[L - k2], b = rb[L - k2];
-            z[k2] = make_float2(a.x + b.y, b.x - a.y);
+        for (int k2 = 0; k2 < L; ++k2) {
+            if (k2 <= H2) {
+                const float2 a = ra[k2], b = rb[k2];
+                z[k2] = make_float2(a.x - b.y, a.y + b.x);
+            } else {
+                const float2 a = ra[L - k2], b = rb[L - k2];
+                z[k2] = make_float2(a.x + b.y, b.x - a.y);
+            }
         }
-    }
-    fft<L, true>(z);
-
-    // 3. crop, concatenate, bias, ReLU
-    const int t = t0 + u;
-    if (t >= nt) return;
-    const int b = t % tw;
-    const int rest = t / tw;
-    const int a = rest % th;
-    const int img = rest / th;
-    const float bv = bias ? bias[co] : 0.f;
-    const int c0 = b * T;
-#pragma unroll
-    for (int rr = 0; rr < 2; ++rr) {
-        const int m = 2 * j + rr;
-        const int r = a * T + m;
-        if (m >= T || r >= h) continue;
-        float* dst = y + ((size_t(img) * cout + co) * h + r) * size_t(w) + c0;
+        fft<L, true>(z);
+        __syncthreads();  // the staged tiles reuse the half-spectrum LDS
+        float* s0 = st + u * STS + 2 * j * SP;
 #pragma unroll
         for (int q = 0; q < L; ++q) {
-            if (q < T && c0 + q < w) {
-                float v = (rr ? z[q].y : z[q].x) + bv;
-                if (relu) v = fmaxf(v, 0.f);
-                dst[q] = v;
+            s0[q] = z[q].x;
+            s0[SP + q] = z[q].y;
+        }
+    }
+    __syncthreads();
+
+    // 3. crop + concatenate + bias + ReLU: lanes (q, u_sub, m_sub), q fastest
+    {
+        const int q = tid % L;
+        const int us = (tid / L) % S::US;
+        const int ms = tid / (L * S::US);
+        const float bv = bias ? bias[co] : 0.f;
+#pragma unroll 4
+        for (int ub = 0; ub < TG; ub += S::US) {
+            const int u = ub + us;
+            const int ro = rows_ok[u], cw = cols_ok[u];
+            float* d = dst_base[u];
+            const float* s = st + u * STS;
+#pragma unroll
+            for (int mb = 0; mb < L; mb += S::MS) {
+                const int m = mb + ms;
+                if (m < ro && q < cw) {
+                    float v = s[m * SP + q] + bv;
+                    if (relu) v = fmaxf(v, 0.f);
+                    d[size_t(m) * w + q] = v;
+                }
             }
         }
     }
@@ -118,10 +176,14 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_os_kernel(const float2* 
 template <int L, int TG>
 static hipError_t launch_inverse_L(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y,
                                    hipStream_t s) {
-    const dim3 grid(p.ntp / TG, p.prob.cout);
-    const dim3 block(TG * (L / 2));
-    hipLaunchKernelGGL((inverse_os_kernel<L, TG>), grid, block, 0, s, ys, bias, y, p.prob.cout, p.coutp, p.prob.h,
-                       p.prob.w, p.T, p.th, p.tw, p.nt, p.ntp, int(p.relu));
+    using S = InvShape<L, TG>;
+    auto kern = inverse_os_kernel<L, TG>;
+    static hipError_t attr = allow_dynamic_lds(kern, S::LDS_BYTES);
+    if (attr != hipSuccess) return attr;
+    const int ngroups = p.ntp / TG;
+    const dim3 grid(unsigned(ngroups) * unsigned(p.prob.cout));
+    hipLaunchKernelGGL(kern, grid, dim3(S::NT), S::LDS_BYTES, s, ys, bias, y, p.prob.cout, p.coutp, p.prob.h,
+                       p.prob.w, p.T, p.th, p.tw, p.nt, p.ntp, ngroups, int(p.relu));
     return hipGetLastError();
 }
 
@@ -130,9 +192,9 @@ hipError_t launch_inverse(const fftsplit_plan_s& p, const float2* ys, const floa
     (void)aux;
     if (p.oaa) return hipErrorNotSupported;
     switch (p.L) {
-        case 8: return launch_inverse_L<8, 32>(p, ys, bias, y, s);
-        case 16: return launch_inverse_L<16, 16>(p, ys, bias, y, s);
-        case 32: return launch_inverse_L<32, 8>(p, ys, bias, y, s);
+        case 8: return launch_inverse_L<8, 64>(p, ys, bias, y, s);
+        case 16: return launch_inverse_L<16, 32>(p, ys, bias, y, s);
+        case 32: return launch_inverse_L<32, 16>(p, ys, bias, y, s);
     }
     return hipErrorInvalidValue;
 }

@@ -84,6 +84,8 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     if (p.stride != 1) return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "only stride 1 is supported");
     if (p.pad != p.k / 2) return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "only 'same' padding (pad = k/2) is supported");
     if (p.k > 31) return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "kernel larger than the largest FFT size");
+    if (size_t(p.h) * size_t(p.w) > size_t(INT_MAX))
+        return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "image planes above 2^31 pixels are not supported");
     if (p.cin > 65535 || p.cout > 65535)
         return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "channel counts above 65535 are not supported");
     const bool oaa = (p.flags & FFTSPLIT_OVERLAP_ADD) != 0;
