@@ -46,12 +46,12 @@ __global__ __launch_bounds__(TG * (L / 2)) void forward_kernel(const float* __re
                                                                int cin, int h, int w, int T, int P, int th, int tw,
                                                                int nt, int ntp, int ngroups) {
     using S = FwdShape<L, TG>;
-    constexpr int H2 = S::H2, NT = S::NT, WP = S::WP, WTS = S::WTS, TP = S::TP, TTS = S::TTS;
+    constexpr int H2 = S::H2, WP = S::WP, WTS = S::WTS, TP = S::TP, TTS = S::TTS;
+    constexpr int RPI = 64 / L;               // window rows per wave-wide load
+    constexpr int TPW = TG / (S::NT / 64);    // patches per wave
     extern __shared__ float4 lds_raw[];
     float* win = reinterpret_cast<float*>(lds_raw);
     float2* tb = reinterpret_cast<float2*>(lds_raw);
-    __shared__ const float* plane[TG];
-    __shared__ int org_r[TG], org_c[TG];
 
     const int tid = threadIdx.x;
     const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
@@ -59,49 +59,47 @@ __global__ __launch_bounds__(TG * (L / 2)) void forward_kernel(const float* __re
     const int c = lb / ngroups;
     const int t0 = g * TG;
 
-    if (tid < TG) {
-        const int t = t0 + tid;
-        int r0 = -(1 << 29), c0 = 0;   // padding patches: every row is out of range
-        const float* base = x;
-        if (t < nt) {
-            const int b = t % tw;
-            const int rest = t / tw;
-            const int a = rest % th;
-            const int img = rest / th;
-            r0 = OAA ? a * T : a * T - P;
-            c0 = OAA ? b * T : b * T - P;
-            base = x + (size_t(img) * cin + c) * size_t(h) * size_t(w);
-        }
-        plane[tid] = base;
-        org_r[tid] = r0;
-        org_c[tid] = c0;
-    }
-    __syncthreads();
-
-    // 1. gather (element e = (u, m, q), q fastest; q is fixed per thread)
+    // 1. gather.  Wave wv reads the windows of its own TPW patches; each
+    // wave-wide load covers RPI consecutive window rows of one patch (L
+    // consecutive lanes per row), so the patch geometry is wave-uniform.
     {
-        const int q = tid % L;
+        const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+        const int lane = tid & 63;
+        const int q = lane % L;
+        const int mr = lane / L;
         float v[S::NLOAD];
 #pragma unroll
-        for (int i = 0; i < S::NLOAD; ++i) {
-            const int e = i * NT + tid;
-            const int m = (e / L) % L;
-            const int u = e / (L * L);
-            int r = org_r[u] + m;
-            int col = org_c[u] + q;
-            bool ok = unsigned(r) < unsigned(h) && unsigned(col) < unsigned(w);
-            if (OAA) ok = ok && m < T && q < T;
-            r = min(max(r, 0), h - 1);
-            col = min(max(col, 0), w - 1);
-            const float val = plane[u][r * w + col];
-            v[i] = ok ? val : 0.f;
+        for (int pi = 0; pi < TPW; ++pi) {
+            const int u = wv * TPW + pi;
+            const int t = t0 + u;
+            int r0 = -(1 << 29), c0 = 0, base = 0;   // padding patches read nothing
+            if (t < nt) {
+                const int b = t % tw;
+                const int rest = t / tw;
+                const int a = rest % th;
+                const int img = rest / th;
+                r0 = OAA ? a * T : a * T - P;
+                c0 = OAA ? b * T : b * T - P;
+                base = (img * cin + c) * h * w;
+            }
+#pragma unroll
+            for (int ri = 0; ri < L / RPI; ++ri) {
+                const int m = ri * RPI + mr;
+                int r = r0 + m;
+                int col = c0 + q;
+                bool ok = unsigned(r) < unsigned(h) && unsigned(col) < unsigned(w);
+                if (OAA) ok = ok && m < T && q < T;
+                r = min(max(r, 0), h - 1);
+                col = min(max(col, 0), w - 1);
+                const float val = x[base + r * w + col];
+                v[pi * (L / RPI) + ri] = ok ? val : 0.f;
+            }
         }
 #pragma unroll
-        for (int i = 0; i < S::NLOAD; ++i) {
-            const int e = i * NT + tid;
-            const int m = (e / L) % L;
-            const int u = e / (L * L);
-            win[u * WTS + m * WP + q] = v[i];
+        for (int pi = 0; pi < TPW; ++pi) {
+            const int u = wv * TPW + pi;
+#pragma unroll
+            for (int ri = 0; ri < L / RPI; ++ri) win[u * WTS + (ri * RPI + mr) * WP + q] = v[pi * (L / RPI) + ri];
         }
     }
     __syncthreads();

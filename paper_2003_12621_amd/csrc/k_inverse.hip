@@ -50,7 +50,7 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_os_kernel(const float2* 
     extern __shared__ float4 lds_raw[];
     float2* tb = reinterpret_cast<float2*>(lds_raw);
     float* st = reinterpret_cast<float*>(lds_raw);
-    __shared__ float* dst_base[TG];
+    __shared__ int dst_off[TG];
     __shared__ int rows_ok[TG], cols_ok[TG];
 
     const int tid = threadIdx.x;
@@ -61,8 +61,7 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_os_kernel(const float2* 
 
     if (tid < TG) {
         const int t = t0 + tid;
-        int ro = 0, cw = 0;
-        float* d = y;
+        int ro = 0, cw = 0, off = 0;
         if (t < nt) {
             const int b = t % tw;
             const int rest = t / tw;
@@ -70,9 +69,9 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_os_kernel(const float2* 
             const int img = rest / th;
             ro = min(T, h - a * T);
             cw = min(T, w - b * T);
-            d = y + ((size_t(img) * cout + co) * h + size_t(a) * T) * size_t(w) + size_t(b) * T;
+            off = ((img * cout + co) * h + a * T) * w + b * T;
         }
-        dst_base[tid] = d;
+        dst_off[tid] = off;
         rows_ok[tid] = ro;
         cols_ok[tid] = cw;
     }
@@ -158,7 +157,7 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_os_kernel(const float2* 
         for (int ub = 0; ub < TG; ub += S::US) {
             const int u = ub + us;
             const int ro = rows_ok[u], cw = cols_ok[u];
-            float* d = dst_base[u];
+            const int d = dst_off[u];
             const float* s = st + u * STS;
 #pragma unroll
             for (int mb = 0; mb < L; mb += S::MS) {
@@ -166,7 +165,7 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_os_kernel(const float2* 
                 if (m < ro && q < cw) {
                     float v = s[m * SP + q] + bv;
                     if (relu) v = fmaxf(v, 0.f);
-                    d[size_t(m) * w + q] = v;
+                    y[d + m * w + q] = v;
                 }
             }
         }

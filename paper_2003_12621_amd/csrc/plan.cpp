@@ -131,10 +131,13 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
         !mul_ok(size_t(g.bins) * 8, size_t(g.coutp), &tmp) || !mul_ok(tmp, size_t(g.ntp), &ys) ||
         !mul_ok(size_t(g.bins) * 8, size_t(p.cin), &tmp) || !mul_ok(tmp, size_t(g.coutp), &wsb))
         return fail(FFTSPLIT_ERROR_INVALID_VALUE, "buffer sizes overflow size_t");
+    // Kernels address x and y with 32-bit element offsets.
     size_t img_elems;
     if (!mul_ok(size_t(p.n) * size_t(p.h), size_t(p.w), &tmp) ||
         !mul_ok(tmp, size_t(p.cin > p.cout ? p.cin : p.cout), &img_elems))
         return fail(FFTSPLIT_ERROR_INVALID_VALUE, "tensor sizes overflow size_t");
+    if (img_elems > size_t(INT_MAX))
+        return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "input/output tensors above 2^31 elements are not supported");
 
     // Architecture check.
     char archbuf[64] = {0};
