@@ -14,12 +14,16 @@
 // channel row, and every stored output row is 32 consecutive patches.
 //
 // Workgroup tile: BM output channels x BN patches of one bin, 4 waves in a
-// 2 x 2 grid.  The input-channel loop runs in stages of KC channels; stage
-// s+1 is loaded from memory into registers while stage s is multiplied out
-// of LDS, then written to the other LDS buffer (one barrier per stage).
-// The channel blocks of one bin are consecutive logical workgroups on the
-// same XCD, so the bin's patch spectra are fetched from HBM once and reused
-// from that die's L2.
+// WM x (4/WM) grid.  The input-channel loop runs in stages of KC channels;
+// stage s+1 is loaded from memory into registers while stage s is
+// multiplied out of LDS, then written to the other LDS buffer (one barrier
+// per stage).  Inside a stage the operand fragments of the next channel
+// pair are read from LDS while the current pair's MFMAs run.  The channel
+// blocks of one bin are consecutive logical workgroups on the same XCD, so
+// the bin's patch spectra are fetched from HBM once and reused from L2.
+#include <cstdlib>
+#include <cstring>
+
 #include "fftsplit_internal.hpp"
 #include "launch_util.hpp"
 
@@ -27,32 +31,35 @@ namespace fftsplit {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-template <int BM, int BN, int KC>
+template <int BM, int BN, int KC, int WM>
 struct ConShape {
     static constexpr int NT = 256;
-    static constexpr int TM = BM / 64;           // 32-row MFMA tiles per wave (2 waves along co)
-    static constexpr int TN = BN / 64;           // 32-col MFMA tiles per wave (2 waves along t)
+    static constexpr int WN = 4 / WM;
+    static constexpr int TM = BM / WM / 32;      // 32-row MFMA tiles per wave
+    static constexpr int TN = BN / WN / 32;      // 32-col MFMA tiles per wave
     static constexpr int WE = KC * BM;           // W stage elements (complex)
     static constexpr int XE = KC * BN;           // X stage elements (complex)
     static constexpr int WL = WE / 2 / NT;       // 16-byte loads per thread per stage
     static constexpr int XL = XE / 2 / NT;
     static constexpr int LDS_BYTES = 2 * (WE + XE) * 8;
+    static_assert(WM * WN == 4, "four waves");
     static_assert(TM >= 1 && TN >= 1 && WL >= 1 && XL >= 1, "tile shape");
     static_assert((WE / 2) % NT == 0 && (XE / 2) % NT == 0, "loads divide evenly");
 };
 
-template <int BM, int BN, int KC>
+template <int BM, int BN, int KC, int WM>
 __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict__ xs, const float2* __restrict__ ws,
                                                        float2* __restrict__ ys, int cin, int coutp, int ntp,
                                                        int nbco, int nbt) {
-    using S = ConShape<BM, BN, KC>;
+    using S = ConShape<BM, BN, KC, WM>;
+    constexpr int TM = S::TM, TN = S::TN;
     extern __shared__ float4 lds_raw[];
     float2* lds = reinterpret_cast<float2*>(lds_raw);   // [2][WE + XE]
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / S::WN, wn = wave % S::WN;
 
     const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
     const int cbk = lb % nbco;
@@ -66,39 +73,57 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     const float4* xsrc = reinterpret_cast<const float4*>(xs + size_t(f) * cin * ntp + t0);
     const int wrow4 = coutp / 2, xrow4 = ntp / 2;   // row pitch in float4
 
-    float4 wreg[S::WL], xreg[S::XL];
+    uint4 wreg[S::WL], xreg[S::XL];
+    // A full stage is loaded as is; only a stage that runs past cin reads
+    // its missing rows from row cin-1 (always in range) and zeroes them.
+    // The branch is uniform, and in the full case the loaded registers are
+    // first used when the stage is written to LDS after the MFMAs, so the
+    // loads stay in flight during the multiply.
     auto load_stage = [&](int k0) {
+        if (k0 + KC <= cin) {
 #pragma unroll
-        for (int i = 0; i < S::WL; ++i) {
-            const int e = i * S::NT + tid;
-            const int kk = e / (BM / 2), c2 = e % (BM / 2);
-            const int ci = k0 + kk;
-            const float4 v = wsrc[size_t(min(ci, cin - 1)) * wrow4 + c2];
-            wreg[i] = ci < cin ? v : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+            for (int i = 0; i < S::WL; ++i) {
+                const int e = i * S::NT + tid;
+                wreg[i] = reinterpret_cast<const uint4*>(wsrc)[(k0 + e / (BM / 2)) * wrow4 + e % (BM / 2)];
+            }
 #pragma unroll
-        for (int i = 0; i < S::XL; ++i) {
-            const int e = i * S::NT + tid;
-            const int kk = e / (BN / 2), c2 = e % (BN / 2);
-            const int ci = k0 + kk;
-            const float4 v = xsrc[size_t(min(ci, cin - 1)) * xrow4 + c2];
-            xreg[i] = ci < cin ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int i = 0; i < S::XL; ++i) {
+                const int e = i * S::NT + tid;
+                xreg[i] = reinterpret_cast<const uint4*>(xsrc)[(k0 + e / (BN / 2)) * xrow4 + e % (BN / 2)];
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < S::WL; ++i) {
+                const int e = i * S::NT + tid;
+                const int ci = k0 + e / (BM / 2);
+                const uint4 v = reinterpret_cast<const uint4*>(wsrc)[min(ci, cin - 1) * wrow4 + e % (BM / 2)];
+                const unsigned m = ci < cin ? 0xffffffffu : 0u;
+                wreg[i] = make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
+            }
+#pragma unroll
+            for (int i = 0; i < S::XL; ++i) {
+                const int e = i * S::NT + tid;
+                const int ci = k0 + e / (BN / 2);
+                const uint4 v = reinterpret_cast<const uint4*>(xsrc)[min(ci, cin - 1) * xrow4 + e % (BN / 2)];
+                const unsigned m = ci < cin ? 0xffffffffu : 0u;
+                xreg[i] = make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
+            }
         }
     };
     auto store_stage = [&](int buf) {
-        float4* sw = reinterpret_cast<float4*>(lds + buf * (S::WE + S::XE));
-        float4* sx = reinterpret_cast<float4*>(lds + buf * (S::WE + S::XE) + S::WE);
+        uint4* sw = reinterpret_cast<uint4*>(lds + buf * (S::WE + S::XE));
+        uint4* sx = reinterpret_cast<uint4*>(lds + buf * (S::WE + S::XE) + S::WE);
 #pragma unroll
         for (int i = 0; i < S::WL; ++i) sw[i * S::NT + tid] = wreg[i];
 #pragma unroll
         for (int i = 0; i < S::XL; ++i) sx[i * S::NT + tid] = xreg[i];
     };
 
-    floatx16 accR[S::TM][S::TN], accI[S::TM][S::TN];
+    floatx16 accR[TM][TN], accI[TM][TN];
 #pragma unroll
-    for (int i = 0; i < S::TM; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < S::TN; ++j)
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 accR[i][j][r] = 0.f;
@@ -115,24 +140,34 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     for (int s = 0; s < nstage; ++s) {
         const int buf = s & 1;
         if (s + 1 < nstage) load_stage((s + 1) * KC);
-        const float2* sw = lds + buf * (S::WE + S::XE) + wm * (S::TM * 32) + col;
-        const float2* sx = lds + buf * (S::WE + S::XE) + S::WE + wn * (S::TN * 32) + col;
+        const float2* sw = lds + buf * (S::WE + S::XE) + krow * BM + wm * (TM * 32) + col;
+        const float2* sx = lds + buf * (S::WE + S::XE) + S::WE + krow * BN + wn * (TN * 32) + col;
+        float2 a[2][TM], b[2][TN];
 #pragma unroll
-        for (int kk = 0; kk < KC; kk += 2) {
-            float2 a[S::TM], b[S::TN];
+        for (int i = 0; i < TM; ++i) a[0][i] = sw[i * 32];
 #pragma unroll
-            for (int i = 0; i < S::TM; ++i) a[i] = sw[(kk + krow) * BM + i * 32];
+        for (int j = 0; j < TN; ++j) b[0][j] = sx[j * 32];
 #pragma unroll
-            for (int j = 0; j < S::TN; ++j) b[j] = sx[(kk + krow) * BN + j * 32];
+        for (int kp = 0; kp < KC / 2; ++kp) {
+            const int cur = kp & 1;
+            if (kp + 1 < KC / 2) {
 #pragma unroll
-            for (int i = 0; i < S::TM; ++i) {
-                const float nai = -a[i].y;
+                for (int i = 0; i < TM; ++i) a[cur ^ 1][i] = sw[(2 * kp + 2) * BM + i * 32];
 #pragma unroll
-                for (int j = 0; j < S::TN; ++j) {
-                    accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i].x, b[j].x, accR[i][j], 0, 0, 0);
-                    accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(nai, b[j].y, accR[i][j], 0, 0, 0);
-                    accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i].x, b[j].y, accI[i][j], 0, 0, 0);
-                    accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i].y, b[j].x, accI[i][j], 0, 0, 0);
+                for (int j = 0; j < TN; ++j) b[cur ^ 1][j] = sx[(2 * kp + 2) * BN + j * 32];
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const float ar = a[cur][i].x, ai = a[cur][i].y, nai = -ai;
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ar, b[cur][j].x, accR[i][j], 0, 0, 0);
+                    accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ar, b[cur][j].y, accI[i][j], 0, 0, 0);
+                }
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(nai, b[cur][j].y, accR[i][j], 0, 0, 0);
+                    accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ai, b[cur][j].x, accI[i][j], 0, 0, 0);
                 }
             }
         }
@@ -141,11 +176,11 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     }
 
 #pragma unroll
-    for (int i = 0; i < S::TM; ++i) {
+    for (int i = 0; i < TM; ++i) {
 #pragma unroll
-        for (int j = 0; j < S::TN; ++j) {
-            float2* yb = ys + (size_t(f) * coutp + co0 + wm * (S::TM * 32) + i * 32) * ntp + t0 +
-                         wn * (S::TN * 32) + j * 32 + col;
+        for (int j = 0; j < TN; ++j) {
+            float2* yb = ys + (size_t(f) * coutp + co0 + wm * (TM * 32) + i * 32) * ntp + t0 + wn * (TN * 32) +
+                         j * 32 + col;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int ii = 8 * (r >> 2) + 4 * krow + (r & 3);
@@ -155,13 +190,14 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     }
 }
 
-template <int BM, int BN, int KC>
+template <int BM, int BN, int KC, int WM>
 static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, const float2* ws, float2* ys,
                                     hipStream_t s) {
-    using S = ConShape<BM, BN, KC>;
-    auto kern = contract_kernel<BM, BN, KC>;
+    using S = ConShape<BM, BN, KC, WM>;
+    auto kern = contract_kernel<BM, BN, KC, WM>;
     static hipError_t attr = allow_dynamic_lds(kern, S::LDS_BYTES);
     if (attr != hipSuccess) return attr;
+    if (p.coutp % BM != 0 || p.ntp % BN != 0) return hipErrorInvalidValue;
     const int nbco = p.coutp / BM, nbt = p.ntp / BN;
     const size_t nb = size_t(nbco) * nbt * p.bins;
     hipLaunchKernelGGL(kern, dim3(unsigned(nb)), dim3(S::NT), S::LDS_BYTES, s, xs, ws, ys, p.prob.cin, p.coutp, p.ntp,
@@ -169,10 +205,28 @@ static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, 
     return hipGetLastError();
 }
 
+// Tile variants, by name "BMxBNxKC" (wave grid fixed per shape).
+hipError_t launch_contract_variant(const char* v, const fftsplit_plan_s& p, const float2* xs, const float2* ws,
+                                   float2* ys, hipStream_t s) {
+    if (!std::strcmp(v, "64x64x16")) return launch_contract_v<64, 64, 16, 2>(p, xs, ws, ys, s);
+    if (!std::strcmp(v, "64x64x32")) return launch_contract_v<64, 64, 32, 2>(p, xs, ws, ys, s);
+    if (!std::strcmp(v, "128x64x16")) return launch_contract_v<128, 64, 16, 2>(p, xs, ws, ys, s);
+    if (!std::strcmp(v, "128x64x32")) return launch_contract_v<128, 64, 32, 2>(p, xs, ws, ys, s);
+    if (!std::strcmp(v, "64x128x16")) return launch_contract_v<64, 128, 16, 2>(p, xs, ws, ys, s);
+    if (!std::strcmp(v, "128x128x16")) return launch_contract_v<128, 128, 16, 2>(p, xs, ws, ys, s);
+    if (!std::strcmp(v, "256x64x16")) return launch_contract_v<256, 64, 16, 4>(p, xs, ws, ys, s);
+    return hipErrorInvalidValue;
+}
+
 hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xs, const float2* ws, float2* ys,
                            hipStream_t s) {
-    if (p.coutp % 128 == 0) return launch_contract_v<128, 64, 16>(p, xs, ws, ys, s);
-    return launch_contract_v<64, 64, 16>(p, xs, ws, ys, s);
+    // FFTSPLIT_CONTRACT_TILE=BMxBNxKC selects a tile variant (tuning aid).
+    if (const char* v = std::getenv("FFTSPLIT_CONTRACT_TILE")) {
+        if (*v) return launch_contract_variant(v, p, xs, ws, ys, s);
+    }
+    // 64x64 tiles with 16-channel stages measured fastest on every layer
+    // shape tried (small register and LDS footprint: 7 waves per SIMD).
+    return launch_contract_v<64, 64, 16, 2>(p, xs, ws, ys, s);
 }
 
 }  // namespace fftsplit

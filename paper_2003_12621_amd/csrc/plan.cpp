@@ -124,6 +124,10 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
         return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "overlap-add needs tile >= k - 1");
     if (g.nt < 0 || g.ntp < 0 || g.ntp / kTileGranule > INT_MAX / 2)
         return fail(FFTSPLIT_ERROR_INVALID_VALUE, "too many patches");
+    // The contraction indexes one bin's spectra with 32-bit offsets.
+    if (size_t(p.cin) * size_t(g.coutp) > size_t(INT_MAX) || size_t(p.cin) * size_t(g.ntp) > size_t(INT_MAX) ||
+        size_t(g.coutp) * size_t(g.ntp) > size_t(INT_MAX))
+        return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "per-bin spectra above 2^31 elements are not supported");
 
     // Byte sizes with overflow checks.
     size_t xs, ys, wsb, tmp;
