@@ -170,6 +170,16 @@ fftsplit_status_t fftsplit_inverse(fftsplit_plan_t plan, const float* bias, floa
 fftsplit_status_t fftsplit_maxpool2x2(const float* x, float* y, int n, int c, int h, int w,
                                       hipStream_t stream);
 
+/* Benchmark hook (host, per calling thread): until called again with
+ * NULL, NULL, every later fftsplit_transform_weights / fftsplit_conv2d /
+ * stage call made by this thread records `start` (if non-NULL) when its
+ * first kernel begins executing and `stop` (if non-NULL) when its last
+ * kernel ends, using the kernels' own dispatch timestamps
+ * (hipExtLaunchKernel) rather than separate event packets.  The events
+ * must be valid hipEvents created with timing enabled, on the plan's
+ * device.  Always returns FFTSPLIT_SUCCESS. */
+fftsplit_status_t fftsplit_set_timing_events(hipEvent_t start, hipEvent_t stop);
+
 /* Static description of a status code. */
 const char* fftsplit_status_string(fftsplit_status_t status);
 

@@ -76,6 +76,7 @@ _SIGNATURES = {
                                         ctypes.c_size_t, ctypes.c_void_p]),
     "fftsplit_maxpool2x2": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
                                            ctypes.c_int, ctypes.c_int, ctypes.c_void_p]),
+    "fftsplit_set_timing_events": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
     "fftsplit_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "fftsplit_last_error": (ctypes.c_char_p, []),
 }
@@ -247,6 +248,21 @@ class Plan:
         i = self.info
         return wspec.view(_torch().complex64)[: i.bins * self.cin * i.cout_padded].view(i.bins, self.cin,
                                                                                          i.cout_padded)
+
+
+def set_timing_events(start=None, stop=None):
+    """Time this thread's following fftsplit calls with two torch.cuda.Event
+    objects (enable_timing=True), recorded by the kernels' own dispatch
+    timestamps; set_timing_events() turns it off.  Each event must already
+    exist on the device (record it once beforehand)."""
+    def handle(ev):
+        if ev is None:
+            return None
+        h = ev.cuda_event
+        if not h:
+            raise ValueError("event has no device handle yet; record it once first")
+        return ctypes.c_void_p(h)
+    _check(lib().fftsplit_set_timing_events(handle(start), handle(stop)), "fftsplit_set_timing_events")
 
 
 def maxpool2x2(x, out=None):

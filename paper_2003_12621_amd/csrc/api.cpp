@@ -4,10 +4,14 @@
 #include <string>
 
 #include "fftsplit_internal.hpp"
+#include "launch_util.hpp"
 
 using namespace fftsplit;
 
 namespace {
+
+// Timing events set by fftsplit_set_timing_events for this thread.
+thread_local LaunchEvents t_events;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -83,7 +87,7 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_transform_weights(fftsplit_plan_t pla
     if (overlap(w, wb, wspec, plan->wspec_bytes)) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "w overlaps wspec");
     DeviceGuard g(plan->device);
     if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
-    return launched(launch_weights(*plan, w, static_cast<float2*>(wspec), stream), "weight transform launch");
+    return launched(launch_weights(*plan, w, static_cast<float2*>(wspec), stream, t_events), "weight transform launch");
 }
 
 FFTSPLIT_EXPORT fftsplit_status_t fftsplit_forward(fftsplit_plan_t plan, const float* x, void* workspace,
@@ -96,8 +100,9 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_forward(fftsplit_plan_t plan, const f
         return fail(FFTSPLIT_ERROR_INVALID_VALUE, "x overlaps the workspace");
     DeviceGuard g(plan->device);
     if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
-    return launched(launch_forward(*plan, x, reinterpret_cast<float2*>(ws_at(workspace, plan->xspec_off)), stream),
-                    "forward patch transform launch");
+    return launched(
+        launch_forward(*plan, x, reinterpret_cast<float2*>(ws_at(workspace, plan->xspec_off)), stream, t_events),
+        "forward patch transform launch");
 }
 
 FFTSPLIT_EXPORT fftsplit_status_t fftsplit_contract(fftsplit_plan_t plan, const void* wspec, void* workspace,
@@ -112,7 +117,7 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_contract(fftsplit_plan_t plan, const 
     if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
     return launched(launch_contract(*plan, reinterpret_cast<const float2*>(ws_at(workspace, plan->xspec_off)),
                                     static_cast<const float2*>(wspec),
-                                    reinterpret_cast<float2*>(ws_at(workspace, plan->yspec_off)), stream),
+                                    reinterpret_cast<float2*>(ws_at(workspace, plan->yspec_off)), stream, t_events),
                     "contraction launch");
 }
 
@@ -128,7 +133,7 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_inverse(fftsplit_plan_t plan, const f
     DeviceGuard g(plan->device);
     if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
     return launched(launch_inverse(*plan, reinterpret_cast<const float2*>(ws_at(workspace, plan->yspec_off)), bias, y,
-                                   plan->aux_bytes ? ws_at(workspace, plan->aux_off) : nullptr, stream),
+                                   plan->aux_bytes ? ws_at(workspace, plan->aux_off) : nullptr, stream, t_events),
                     "inverse patch transform launch");
 }
 
@@ -151,12 +156,16 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_conv2d(fftsplit_plan_t plan, const fl
     if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
     float2* xs = reinterpret_cast<float2*>(ws_at(workspace, plan->xspec_off));
     float2* ys = reinterpret_cast<float2*>(ws_at(workspace, plan->yspec_off));
-    if (fftsplit_status_t s = launched(launch_forward(*plan, x, xs, stream), "forward patch transform launch")) return s;
-    if (fftsplit_status_t s = launched(launch_contract(*plan, xs, static_cast<const float2*>(wspec), ys, stream),
+    LaunchEvents first, middle, last;
+    first.start = t_events.start;
+    last.stop = t_events.stop;
+    if (fftsplit_status_t s = launched(launch_forward(*plan, x, xs, stream, first), "forward patch transform launch"))
+        return s;
+    if (fftsplit_status_t s = launched(launch_contract(*plan, xs, static_cast<const float2*>(wspec), ys, stream, middle),
                                        "contraction launch"))
         return s;
     return launched(launch_inverse(*plan, ys, bias, y, plan->aux_bytes ? ws_at(workspace, plan->aux_off) : nullptr,
-                                   stream),
+                                   stream, last),
                     "inverse patch transform launch");
 }
 
@@ -169,4 +178,11 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_maxpool2x2(const float* x, float* y, 
     const size_t xb = size_t(n) * c * h * w * 4, yb = size_t(n) * c * (h / 2) * (w / 2) * 4;
     if (overlap(x, xb, y, yb)) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "y overlaps x");
     return launched(launch_maxpool(x, y, n, c, h, w, stream), "max-pool launch");
+}
+
+FFTSPLIT_EXPORT fftsplit_status_t fftsplit_set_timing_events(hipEvent_t start, hipEvent_t stop) {
+    set_error("");
+    t_events.start = start;
+    t_events.stop = stop;
+    return FFTSPLIT_SUCCESS;
 }

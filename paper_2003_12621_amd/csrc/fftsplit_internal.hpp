@@ -41,13 +41,17 @@ __host__ __device__ constexpr int bin_colh(int L, int k1) { return L * (L / 2 - 
 void set_error(const std::string& msg);
 fftsplit_status_t fail(fftsplit_status_t st, const std::string& msg);
 
-// Kernel launchers (one per .hip file); return hipSuccess or the launch error.
-hipError_t launch_weights(const fftsplit_plan_s& p, const float* w, float2* wspec, hipStream_t s);
-hipError_t launch_forward(const fftsplit_plan_s& p, const float* x, float2* xspec, hipStream_t s);
-hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xspec, const float2* wspec,
-                           float2* yspec, hipStream_t s);
-hipError_t launch_inverse(const fftsplit_plan_s& p, const float2* yspec, const float* bias, float* y,
-                          void* aux, hipStream_t s);
+// Kernel launchers (one per .hip file); return hipSuccess or the launch
+// error.  `ev` optionally times the launch sequence (see launch_util.hpp).
+struct LaunchEvents;
+hipError_t launch_weights(const fftsplit_plan_s& p, const float* w, float2* wspec, hipStream_t s,
+                          const LaunchEvents& ev);
+hipError_t launch_forward(const fftsplit_plan_s& p, const float* x, float2* xspec, hipStream_t s,
+                          const LaunchEvents& ev);
+hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xspec, const float2* wspec, float2* yspec,
+                           hipStream_t s, const LaunchEvents& ev);
+hipError_t launch_inverse(const fftsplit_plan_s& p, const float2* yspec, const float* bias, float* y, void* aux,
+                          hipStream_t s, const LaunchEvents& ev);
 hipError_t launch_maxpool(const float* x, float* y, int n, int c, int h, int w, hipStream_t s);
 
 }  // namespace fftsplit

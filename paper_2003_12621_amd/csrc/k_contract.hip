@@ -192,7 +192,7 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
 
 template <int BM, int BN, int KC, int WM>
 static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, const float2* ws, float2* ys,
-                                    hipStream_t s) {
+                                    hipStream_t s, const LaunchEvents& ev) {
     using S = ConShape<BM, BN, KC, WM>;
     auto kern = contract_kernel<BM, BN, KC, WM>;
     static hipError_t attr = allow_dynamic_lds(kern, S::LDS_BYTES);
@@ -200,33 +200,32 @@ static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, 
     if (p.coutp % BM != 0 || p.ntp % BN != 0) return hipErrorInvalidValue;
     const int nbco = p.coutp / BM, nbt = p.ntp / BN;
     const size_t nb = size_t(nbco) * nbt * p.bins;
-    hipLaunchKernelGGL(kern, dim3(unsigned(nb)), dim3(S::NT), S::LDS_BYTES, s, xs, ws, ys, p.prob.cin, p.coutp, p.ntp,
-                       nbco, nbt);
-    return hipGetLastError();
+    return launch_kernel(kern, dim3(unsigned(nb)), dim3(S::NT), S::LDS_BYTES, s, ev.start, ev.stop, xs, ws, ys,
+                         p.prob.cin, p.coutp, p.ntp, nbco, nbt);
 }
 
 // Tile variants, by name "BMxBNxKC" (wave grid fixed per shape).
 hipError_t launch_contract_variant(const char* v, const fftsplit_plan_s& p, const float2* xs, const float2* ws,
-                                   float2* ys, hipStream_t s) {
-    if (!std::strcmp(v, "64x64x16")) return launch_contract_v<64, 64, 16, 2>(p, xs, ws, ys, s);
-    if (!std::strcmp(v, "64x64x32")) return launch_contract_v<64, 64, 32, 2>(p, xs, ws, ys, s);
-    if (!std::strcmp(v, "128x64x16")) return launch_contract_v<128, 64, 16, 2>(p, xs, ws, ys, s);
-    if (!std::strcmp(v, "128x64x32")) return launch_contract_v<128, 64, 32, 2>(p, xs, ws, ys, s);
-    if (!std::strcmp(v, "64x128x16")) return launch_contract_v<64, 128, 16, 2>(p, xs, ws, ys, s);
-    if (!std::strcmp(v, "128x128x16")) return launch_contract_v<128, 128, 16, 2>(p, xs, ws, ys, s);
-    if (!std::strcmp(v, "256x64x16")) return launch_contract_v<256, 64, 16, 4>(p, xs, ws, ys, s);
+                                   float2* ys, hipStream_t s, const LaunchEvents& ev) {
+    if (!std::strcmp(v, "64x64x16")) return launch_contract_v<64, 64, 16, 2>(p, xs, ws, ys, s, ev);
+    if (!std::strcmp(v, "64x64x32")) return launch_contract_v<64, 64, 32, 2>(p, xs, ws, ys, s, ev);
+    if (!std::strcmp(v, "128x64x16")) return launch_contract_v<128, 64, 16, 2>(p, xs, ws, ys, s, ev);
+    if (!std::strcmp(v, "128x64x32")) return launch_contract_v<128, 64, 32, 2>(p, xs, ws, ys, s, ev);
+    if (!std::strcmp(v, "64x128x16")) return launch_contract_v<64, 128, 16, 2>(p, xs, ws, ys, s, ev);
+    if (!std::strcmp(v, "128x128x16")) return launch_contract_v<128, 128, 16, 2>(p, xs, ws, ys, s, ev);
+    if (!std::strcmp(v, "256x64x16")) return launch_contract_v<256, 64, 16, 4>(p, xs, ws, ys, s, ev);
     return hipErrorInvalidValue;
 }
 
 hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xs, const float2* ws, float2* ys,
-                           hipStream_t s) {
+                           hipStream_t s, const LaunchEvents& ev) {
     // FFTSPLIT_CONTRACT_TILE=BMxBNxKC selects a tile variant (tuning aid).
     if (const char* v = std::getenv("FFTSPLIT_CONTRACT_TILE")) {
-        if (*v) return launch_contract_variant(v, p, xs, ws, ys, s);
+        if (*v) return launch_contract_variant(v, p, xs, ws, ys, s, ev);
     }
     // 64x64 tiles with 16-channel stages measured fastest on every layer
     // shape tried (small register and LDS footprint: 7 waves per SIMD).
-    return launch_contract_v<64, 64, 16, 2>(p, xs, ws, ys, s);
+    return launch_contract_v<64, 64, 16, 2>(p, xs, ws, ys, s, ev);
 }
 
 }  // namespace fftsplit

@@ -158,28 +158,30 @@ __global__ __launch_bounds__(TG * (L / 2)) void forward_kernel(const float* __re
 }
 
 template <int L, int TG, bool OAA>
-static hipError_t launch_forward_v(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s) {
+static hipError_t launch_forward_v(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s,
+                                   const LaunchEvents& ev) {
     using S = FwdShape<L, TG>;
     auto kern = forward_kernel<L, TG, OAA>;
     static hipError_t attr = allow_dynamic_lds(kern, S::LDS_BYTES);
     if (attr != hipSuccess) return attr;
     const int ngroups = p.ntp / TG;
     const dim3 grid(unsigned(ngroups) * unsigned(p.prob.cin));
-    hipLaunchKernelGGL(kern, grid, dim3(S::NT), S::LDS_BYTES, s, x, xs, p.prob.cin, p.prob.h, p.prob.w, p.T, p.P,
-                       p.th, p.tw, p.nt, p.ntp, ngroups);
-    return hipGetLastError();
+    return launch_kernel(kern, grid, dim3(S::NT), S::LDS_BYTES, s, ev.start, ev.stop, x, xs, p.prob.cin, p.prob.h,
+                         p.prob.w, p.T, p.P, p.th, p.tw, p.nt, p.ntp, ngroups);
 }
 
 template <int L, int TG>
-static hipError_t launch_forward_L(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s) {
-    return p.oaa ? launch_forward_v<L, TG, true>(p, x, xs, s) : launch_forward_v<L, TG, false>(p, x, xs, s);
+static hipError_t launch_forward_L(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s,
+                                   const LaunchEvents& ev) {
+    return p.oaa ? launch_forward_v<L, TG, true>(p, x, xs, s, ev) : launch_forward_v<L, TG, false>(p, x, xs, s, ev);
 }
 
-hipError_t launch_forward(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s) {
+hipError_t launch_forward(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s,
+                          const LaunchEvents& ev) {
     switch (p.L) {
-        case 8: return launch_forward_L<8, 64>(p, x, xs, s);
-        case 16: return launch_forward_L<16, 32>(p, x, xs, s);
-        case 32: return launch_forward_L<32, 16>(p, x, xs, s);
+        case 8: return launch_forward_L<8, 64>(p, x, xs, s, ev);
+        case 16: return launch_forward_L<16, 32>(p, x, xs, s, ev);
+        case 32: return launch_forward_L<32, 16>(p, x, xs, s, ev);
     }
     return hipErrorInvalidValue;
 }

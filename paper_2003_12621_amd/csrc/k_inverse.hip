@@ -174,26 +174,25 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_os_kernel(const float2* 
 
 template <int L, int TG>
 static hipError_t launch_inverse_L(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y,
-                                   hipStream_t s) {
+                                   hipStream_t s, const LaunchEvents& ev) {
     using S = InvShape<L, TG>;
     auto kern = inverse_os_kernel<L, TG>;
     static hipError_t attr = allow_dynamic_lds(kern, S::LDS_BYTES);
     if (attr != hipSuccess) return attr;
     const int ngroups = p.ntp / TG;
     const dim3 grid(unsigned(ngroups) * unsigned(p.prob.cout));
-    hipLaunchKernelGGL(kern, grid, dim3(S::NT), S::LDS_BYTES, s, ys, bias, y, p.prob.cout, p.coutp, p.prob.h,
-                       p.prob.w, p.T, p.th, p.tw, p.nt, p.ntp, ngroups, int(p.relu));
-    return hipGetLastError();
+    return launch_kernel(kern, grid, dim3(S::NT), S::LDS_BYTES, s, ev.start, ev.stop, ys, bias, y, p.prob.cout,
+                         p.coutp, p.prob.h, p.prob.w, p.T, p.th, p.tw, p.nt, p.ntp, ngroups, int(p.relu));
 }
 
 hipError_t launch_inverse(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y, void* aux,
-                          hipStream_t s) {
+                          hipStream_t s, const LaunchEvents& ev) {
     (void)aux;
     if (p.oaa) return hipErrorNotSupported;
     switch (p.L) {
-        case 8: return launch_inverse_L<8, 64>(p, ys, bias, y, s);
-        case 16: return launch_inverse_L<16, 32>(p, ys, bias, y, s);
-        case 32: return launch_inverse_L<32, 16>(p, ys, bias, y, s);
+        case 8: return launch_inverse_L<8, 64>(p, ys, bias, y, s, ev);
+        case 16: return launch_inverse_L<16, 32>(p, ys, bias, y, s, ev);
+        case 32: return launch_inverse_L<32, 16>(p, ys, bias, y, s, ev);
     }
     return hipErrorInvalidValue;
 }

@@ -9,6 +9,7 @@
 // inverse transform's 1/L^2 is folded in here so the hot path never scales.
 #include "fftsplit_internal.hpp"
 #include "fft_regs.hpp"
+#include "launch_util.hpp"
 
 namespace fftsplit {
 
@@ -60,7 +61,8 @@ __global__ __launch_bounds__(256) void weights_kernel(const float* __restrict__ 
     wspec[idx] = make_float2(float(re * inv), float(im * inv));
 }
 
-hipError_t launch_weights(const fftsplit_plan_s& p, const float* w, float2* wspec, hipStream_t s) {
+hipError_t launch_weights(const fftsplit_plan_s& p, const float* w, float2* wspec, hipStream_t s,
+                          const LaunchEvents& ev) {
     TwiddlesD tw;
     for (int i = 0; i < kTwN; ++i) {
         tw.c[i] = kTwCosD[i];
@@ -68,9 +70,8 @@ hipError_t launch_weights(const fftsplit_plan_s& p, const float* w, float2* wspe
     }
     const size_t total = size_t(p.bins) * p.prob.cin * p.coutp;
     const unsigned blocks = unsigned((total + 255) / 256);
-    hipLaunchKernelGGL(weights_kernel, dim3(blocks), dim3(256), 0, s, w, wspec, p.prob.cin, p.prob.cout, p.coutp,
-                       p.prob.k, p.L, p.bins, tw);
-    return hipGetLastError();
+    return launch_kernel(weights_kernel, dim3(blocks), dim3(256), 0, s, ev.start, ev.stop, w, wspec, p.prob.cin,
+                         p.prob.cout, p.coutp, p.prob.k, p.L, p.bins, tw);
 }
 
 }  // namespace fftsplit

@@ -1,6 +1,7 @@
 // Launch helpers shared by the kernel files.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 namespace fftsplit {
@@ -26,6 +27,24 @@ inline hipError_t allow_dynamic_lds(K kernel, int bytes) {
     if (bytes <= 64 * 1024) return hipSuccess;
     return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
                                bytes);
+}
+
+// Optional timing events of one entry-point call: `start` is recorded when
+// the call's first kernel begins and `stop` when its last kernel ends
+// (hipExtLaunchKernel timestamps, no separate event packets).
+struct LaunchEvents {
+    hipEvent_t start = nullptr;
+    hipEvent_t stop = nullptr;
+};
+
+template <typename K, typename... Args>
+inline hipError_t launch_kernel(K kernel, dim3 grid, dim3 block, unsigned lds, hipStream_t s, hipEvent_t start,
+                                hipEvent_t stop, Args... args) {
+    if (start || stop)
+        hipExtLaunchKernelGGL(kernel, grid, block, lds, s, start, stop, 0, args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, lds, s, args...);
+    return hipGetLastError();
 }
 
 }  // namespace fftsplit

@@ -145,3 +145,26 @@ def test_error_paths():
     torch.cuda.synchronize()
     assert rel_l2(y.cpu().numpy(), oracle.direct_xcorr2d(x, w)) <= GATE
 
+
+
+def test_timing_events_bracket_the_kernels():
+    x, w = small_layer(2, 16, 40, 40, 32, 3, seed=61)
+    plan = fs.Plan(2, 16, 40, 40, 32, 3, tile=14)
+    wspec = plan.transform_weights(_dev(w))
+    xd = _dev(x)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in ev:
+        e.record()
+    ws = plan.new_workspace()
+    fs.set_timing_events(ev[0], ev[1])
+    y = plan.conv2d(xd, wspec, workspace=ws)
+    fs.set_timing_events(ev[2], ev[3])
+    plan.contract(wspec, ws)
+    fs.set_timing_events()
+    torch.cuda.synchronize()
+    t_conv = ev[0].elapsed_time(ev[1])
+    t_con = ev[2].elapsed_time(ev[3])
+    assert 0 < t_con < t_conv < 1000.0
+    assert rel_l2(y.cpu().numpy(), oracle.direct_xcorr2d(x, w)) <= GATE
+    with pytest.raises(ValueError):
+        fs.set_timing_events(torch.cuda.Event(enable_timing=True), None)
