@@ -79,18 +79,19 @@ def cpu_baseline(layer, x, w, b, tile, budget_s=12.0):
                       f"{cores} host cores visible, BLAS threads {blas_threads}"}
 
 
-def load_traffic(kernel_tag):
-    """HBM traffic per launch from a committed rocprofv3 --pmc summary, if it
-    was taken on the current kernel sources; otherwise None."""
+def load_traffic(kernel, workload_tag):
+    """HBM bytes per launch of `kernel` on this workload, from the committed
+    rocprofv3 --pmc summary (profiles/traffic.json), if it was taken on the
+    kernel's current sources; otherwise None."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     try:
-        rec = json.load(open(path)).get(kernel_tag)
+        rec = json.load(open(path)).get(f"{kernel}:{workload_tag}")
         if not rec:
             return None
         from paper_2003_12621_amd.build import source_digest
-        if rec.get("source_digest") != source_digest():
+        if rec.get("source_digest") != source_digest(kernel):
             return None
         return rec.get("bytes_per_launch")
     except Exception:
@@ -200,7 +201,8 @@ def main():
         got = y.cpu().numpy()[imgs][:, sel].astype(np.float64)
         parity = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
 
-    traffic = load_traffic(f"contract_{args.config}_T{tile}_{args.mode}")
+    wtag = f"{args.config}_T{tile}_{args.mode}"
+    traffic = load_traffic("contract", wtag)
     out = {
         "metric": "effective direct-conv GFLOP/s",
         "value": round(value, 1),
@@ -224,12 +226,14 @@ def main():
                      "frac": round(con_tfs / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": traffic},
         "stages": {
             "forward": {"ms": round(avg(fwd), 4), "GB/s": round(fwd_gbs, 1),
-                        "frac_hbm": round(fwd_gbs / HBM_PEAK_GBS, 4), "bytes": counts["forward_bytes"]},
+                        "frac_hbm": round(fwd_gbs / HBM_PEAK_GBS, 4), "bytes": counts["forward_bytes"],
+                        "traffic": load_traffic("forward", wtag)},
             "contract": {"ms": round(avg(con), 4), "TFLOP/s": round(con_tfs, 2),
                          "frac_mfma": round(con_tfs / FP32_MFMA_PEAK_TFLOPS, 4),
                          "flops": counts["contract_flops"], "bytes": counts["contract_bytes"]},
             "inverse": {"ms": round(avg(inv), 4), "GB/s": round(inv_gbs, 1),
-                        "frac_hbm": round(inv_gbs / HBM_PEAK_GBS, 4), "bytes": counts["inverse_bytes"]},
+                        "frac_hbm": round(inv_gbs / HBM_PEAK_GBS, 4), "bytes": counts["inverse_bytes"],
+                        "traffic": load_traffic("inverse", wtag)},
         },
         "timing": "per-kernel start/stop from dispatch timestamps (hipExtLaunchKernel events); "
                   "ms_per_step spans the first forward start to the last inverse end",

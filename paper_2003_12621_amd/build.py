@@ -61,19 +61,28 @@ def build(verbose: bool = False) -> str:
 
 
 
-def source_digest() -> str:
-    """SHA-256 over the library's sources and headers (identifies a kernel build)."""
+# Sources each timed kernel is compiled from (for profile-record validity).
+KERNEL_SOURCES = {
+    "forward": ["k_forward.hip", "fft_regs.hpp", "twiddles.inc", "launch_util.hpp", "fftsplit_internal.hpp"],
+    "contract": ["k_contract.hip", "launch_util.hpp", "fftsplit_internal.hpp"],
+    "inverse": ["k_inverse.hip", "fft_regs.hpp", "twiddles.inc", "launch_util.hpp", "fftsplit_internal.hpp"],
+}
+
+
+def source_digest(kernel: str = None) -> str:
+    """SHA-256 (16 hex digits) over the sources of one kernel, or of the
+    whole library when `kernel` is None."""
     import hashlib
     h = hashlib.sha256()
-    names = sorted(os.listdir(CSRC))
+    names = KERNEL_SOURCES[kernel] if kernel else sorted(
+        n for n in os.listdir(CSRC) if n.endswith((".hip", ".cpp", ".hpp", ".inc")))
     for name in names:
-        if name.endswith((".hip", ".cpp", ".hpp", ".inc")):
-            with open(os.path.join(CSRC, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
-    with open(os.path.join(ROOT, "include", "fftsplit.h"), "rb") as f:
-        h.update(f.read())
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    if kernel is None:
+        with open(os.path.join(ROOT, "include", "fftsplit.h"), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()[:16]
-
 
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
