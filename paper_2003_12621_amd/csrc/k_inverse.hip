@@ -15,6 +15,15 @@
 //      output tile (the crop), staged in LDS and written back row by row
 //      with bias and ReLU; horizontally adjacent patches of a group land in
 //      one contiguous run of the output row (the concatenation).
+//   3'. overlap-add placement (zero-padded patches): entry (p, q) of a
+//      patch's L x L result belongs at output (aT+P+p', bT+P+q') with
+//      p' = p for p < T and p - L otherwise, so each patch covers the L x L
+//      region around its tile.  Entries with p, q < T-2P (the "core") have
+//      no other contributor and are written directly with bias and ReLU;
+//      the rest (seams, 2P wide, shared by 2 or 4 neighbouring patches) go to
+//      a per-patch L x L slot of the aux buffer, and seam_kernel then sums
+//      the 1-4 contributions of every seam pixel in a fixed order (no
+//      atomics, deterministic) and applies bias and ReLU.
 // The inverse's 1/L^2 is already folded into the filter spectra.
 #include "fftsplit_internal.hpp"
 #include "fft_regs.hpp"
@@ -39,12 +48,12 @@ struct InvShape {
     static_assert(NT % (L * US) == 0 && TG % US == 0 && L % MS == 0, "store-phase lane split");
 };
 
-template <int L, int TG>
-__global__ __launch_bounds__(TG * (L / 2)) void inverse_os_kernel(const float2* __restrict__ ys,
-                                                                  const float* __restrict__ bias,
-                                                                  float* __restrict__ y, int cout, int coutp, int h,
-                                                                  int w, int T, int th, int tw, int nt, int ntp,
-                                                                  int ngroups, int relu) {
+template <int L, int TG, bool OAA>
+__global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __restrict__ ys,
+                                                               const float* __restrict__ bias, float* __restrict__ y,
+                                                               float* __restrict__ aux, int cout, int coutp, int h,
+                                                               int w, int T, int P, int th, int tw, int nt, int ntp,
+                                                               int ngroups, int relu) {
     using S = InvShape<L, TG>;
     constexpr int H2 = S::H2, NT = S::NT, TP = S::TP, TTS = S::TTS, SP = S::SP, STS = S::STS;
     extern __shared__ float4 lds_raw[];
@@ -67,9 +76,11 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_os_kernel(const float2* 
             const int rest = t / tw;
             const int a = rest % th;
             const int img = rest / th;
-            ro = min(T, h - a * T);
-            cw = min(T, w - b * T);
-            off = ((img * cout + co) * h + a * T) * w + b * T;
+            // overlap-save: rows/cols of the crop inside the image;
+            // overlap-add: rows/cols of the core (offset P) inside the image.
+            ro = OAA ? min(T - 2 * P, h - a * T - P) : min(T, h - a * T);
+            cw = OAA ? min(T - 2 * P, w - b * T - P) : min(T, w - b * T);
+            off = ((img * cout + co) * h + a * T) * w + b * T + (OAA ? P * w + P : 0);
         }
         dst_off[tid] = off;
         rows_ok[tid] = ro;
@@ -147,52 +158,121 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_os_kernel(const float2* 
     }
     __syncthreads();
 
-    // 3. crop + concatenate + bias + ReLU: lanes (q, u_sub, m_sub), q fastest
+    // 3. placement: lanes (q, u_sub, m_sub), q fastest
     {
         const int q = tid % L;
         const int us = (tid / L) % S::US;
         const int ms = tid / (L * S::US);
         const float bv = bias ? bias[co] : 0.f;
+        const int cs = T - 2 * P;  // overlap-add core size
 #pragma unroll 4
         for (int ub = 0; ub < TG; ub += S::US) {
             const int u = ub + us;
             const int ro = rows_ok[u], cw = cols_ok[u];
             const int d = dst_off[u];
             const float* s = st + u * STS;
+            if (!OAA) {
 #pragma unroll
-            for (int mb = 0; mb < L; mb += S::MS) {
-                const int m = mb + ms;
-                if (m < ro && q < cw) {
-                    float v = s[m * SP + q] + bv;
-                    if (relu) v = fmaxf(v, 0.f);
-                    y[d + m * w + q] = v;
+                for (int mb = 0; mb < L; mb += S::MS) {
+                    const int m = mb + ms;
+                    if (m < ro && q < cw) {
+                        float v = s[m * SP + q] + bv;
+                        if (relu) v = fmaxf(v, 0.f);
+                        y[d + m * w + q] = v;
+                    }
+                }
+            } else if (t0 + u < nt) {
+                float* slot = aux + (co * ntp + t0 + u) * (L * L);
+#pragma unroll
+                for (int mb = 0; mb < L; mb += S::MS) {
+                    const int m = mb + ms;
+                    const float zv = s[m * SP + q];
+                    if (m < cs && q < cs) {
+                        if (m < ro && q < cw) {
+                            float v = zv + bv;
+                            if (relu) v = fmaxf(v, 0.f);
+                            y[d + m * w + q] = v;
+                        }
+                    } else {
+                        slot[m * L + q] = zv;
+                    }
                 }
             }
         }
     }
 }
 
-template <int L, int TG>
-static hipError_t launch_inverse_L(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y,
-                                   hipStream_t s, const LaunchEvents& ev) {
+// Overlap-add seams: every output pixel within P of a tile boundary (in
+// either direction) sums the aux entries of the 1-4 patches covering it, in
+// the order (a0-1, b0-1), (a0-1, b0), (a0, b0-1), (a0, b0), then adds the
+// bias and applies ReLU.  Core pixels were written by inverse_kernel.
+__global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux, const float* __restrict__ bias,
+                                                   float* __restrict__ y, int cout, int h, int w, int T, int P, int L,
+                                                   int th, int tw, int ntp, int relu) {
+    const int plane = blockIdx.y;
+    const int idx = blockIdx.x * 256 + threadIdx.x;
+    if (idx >= h * w) return;
+    const int r = idx / w, c = idx % w;
+    const bool seam_r = (r + P) % T < 2 * P;
+    const bool seam_c = (c + P) % T < 2 * P;
+    if (!seam_r && !seam_c) return;
+    const int img = plane / cout, co = plane % cout;
+    const int a0 = (r + P) / T, b0 = (c + P) / T;
+    float acc = 0.f;
+#pragma unroll
+    for (int da = 1; da >= 0; --da) {
+        const int a = a0 - da;
+        if ((da && !seam_r) || a < 0 || a >= th) continue;
+        int p = r - a * T - P;
+        if (p < 0) p += L;
+#pragma unroll
+        for (int db = 1; db >= 0; --db) {
+            const int b = b0 - db;
+            if ((db && !seam_c) || b < 0 || b >= tw) continue;
+            int qq = c - b * T - P;
+            if (qq < 0) qq += L;
+            const int t = (img * th + a) * tw + b;
+            acc += aux[((co * ntp + t) * L + p) * L + qq];
+        }
+    }
+    float v = acc + (bias ? bias[co] : 0.f);
+    if (relu) v = fmaxf(v, 0.f);
+    y[(size_t(plane) * h + r) * w + c] = v;
+}
+
+template <int L, int TG, bool OAA>
+static hipError_t launch_inverse_v(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y,
+                                   float* aux, hipStream_t s, const LaunchEvents& ev) {
     using S = InvShape<L, TG>;
-    auto kern = inverse_os_kernel<L, TG>;
+    auto kern = inverse_kernel<L, TG, OAA>;
     static hipError_t attr = allow_dynamic_lds(kern, S::LDS_BYTES);
     if (attr != hipSuccess) return attr;
     const int ngroups = p.ntp / TG;
     const dim3 grid(unsigned(ngroups) * unsigned(p.prob.cout));
-    return launch_kernel(kern, grid, dim3(S::NT), S::LDS_BYTES, s, ev.start, ev.stop, ys, bias, y, p.prob.cout,
-                         p.coutp, p.prob.h, p.prob.w, p.T, p.th, p.tw, p.nt, p.ntp, ngroups, int(p.relu));
+    hipError_t e = launch_kernel(kern, grid, dim3(S::NT), S::LDS_BYTES, s, ev.start, OAA ? nullptr : ev.stop, ys,
+                                 bias, y, aux, p.prob.cout, p.coutp, p.prob.h, p.prob.w, p.T, p.P, p.th, p.tw, p.nt,
+                                 p.ntp, ngroups, int(p.relu));
+    if (e != hipSuccess || !OAA) return e;
+    const dim3 sgrid(unsigned((p.prob.h * p.prob.w + 255) / 256), unsigned(p.prob.n * p.prob.cout));
+    return launch_kernel(seam_kernel, sgrid, dim3(256), 0, s, nullptr, ev.stop, aux, bias, y, p.prob.cout, p.prob.h,
+                         p.prob.w, p.T, p.P, p.L, p.th, p.tw, p.ntp, int(p.relu));
+}
+
+template <int L, int TG>
+static hipError_t launch_inverse_L(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y,
+                                   float* aux, hipStream_t s, const LaunchEvents& ev) {
+    return p.oaa ? launch_inverse_v<L, TG, true>(p, ys, bias, y, aux, s, ev)
+                 : launch_inverse_v<L, TG, false>(p, ys, bias, y, aux, s, ev);
 }
 
 hipError_t launch_inverse(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y, void* aux,
                           hipStream_t s, const LaunchEvents& ev) {
-    (void)aux;
-    if (p.oaa) return hipErrorNotSupported;
+    float* a = static_cast<float*>(aux);
+    if (p.oaa && !a) return hipErrorInvalidValue;
     switch (p.L) {
-        case 8: return launch_inverse_L<8, 64>(p, ys, bias, y, s, ev);
-        case 16: return launch_inverse_L<16, 32>(p, ys, bias, y, s, ev);
-        case 32: return launch_inverse_L<32, 16>(p, ys, bias, y, s, ev);
+        case 8: return launch_inverse_L<8, 64>(p, ys, bias, y, a, s, ev);
+        case 16: return launch_inverse_L<16, 32>(p, ys, bias, y, a, s, ev);
+        case 32: return launch_inverse_L<32, 16>(p, ys, bias, y, a, s, ev);
     }
     return hipErrorInvalidValue;
 }

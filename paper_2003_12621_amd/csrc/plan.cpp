@@ -124,6 +124,9 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
         return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "overlap-add needs tile >= k - 1");
     if (g.nt < 0 || g.ntp < 0 || g.ntp / kTileGranule > INT_MAX / 2)
         return fail(FFTSPLIT_ERROR_INVALID_VALUE, "too many patches");
+    // The overlap-add seam buffer is indexed with 32-bit offsets.
+    if (oaa && size_t(p.cout) * size_t(g.ntp) * size_t(g.L) * size_t(g.L) > size_t(INT_MAX))
+        return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "overlap-add seam buffer above 2^31 elements is not supported");
     // The contraction indexes one bin's spectra with 32-bit offsets.
     if (size_t(p.cin) * size_t(g.coutp) > size_t(INT_MAX) || size_t(p.cin) * size_t(g.ntp) > size_t(INT_MAX) ||
         size_t(g.coutp) * size_t(g.ntp) > size_t(INT_MAX))
@@ -181,7 +184,8 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     plan->yspec_off = round_up(xs, 256);
     plan->yspec_bytes = ys;
     plan->aux_off = round_up(plan->yspec_off + ys, 256);
-    plan->aux_bytes = 0;
+    // Overlap-add keeps each patch's L x L inverse result for the seam pass.
+    plan->aux_bytes = oaa ? size_t(p.cout) * size_t(g.ntp) * size_t(g.L) * size_t(g.L) * 4 : 0;
     plan->ws_bytes = plan->aux_off + plan->aux_bytes;
 
     const char* log = std::getenv("FFTSPLIT_LOG");

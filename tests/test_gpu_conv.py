@@ -39,15 +39,16 @@ def run_layer(x, w, b, tile, mode="os", relu=False):
 def config_cases():
     for name, cfg in CONFIGS.items():
         for t in cfg["tiles"]:
-            yield pytest.param(name, t, id=f"{name}-T{t}")
+            for mode in ("os", "oaa"):
+                yield pytest.param(name, t, mode, id=f"{name}-T{t}-{mode}")
 
 
-@pytest.mark.parametrize("name,tile", list(config_cases()))
-def test_config_parity(name, tile):
+@pytest.mark.parametrize("name,tile,mode", list(config_cases()))
+def test_config_parity(name, tile, mode):
     x, w, b = make_config(name)
     layer = CONFIGS[name]["layer"]
-    print(f"[case] {name} T={tile}", flush=True)
-    plan, y = run_layer(x, w, b, tile)
+    print(f"[case] {name} T={tile} {mode}", flush=True)
+    plan, y = run_layer(x, w, b, tile, mode=mode)
     assert plan.tile == tile
     if layer.direct_flops <= 8e9:
         ref = oracle.direct_xcorr2d(x, w, b)
@@ -58,12 +59,13 @@ def test_config_parity(name, tile):
         ref = oracle.direct_xcorr2d(x, w[sel], None if b is None else b[sel])
         got = y[:, sel]
     err = rel_l2(got, ref)
-    print(f"[case] {name} T={tile} rel_l2={err:.3e} rel_max={rel_max(got, ref):.3e}", flush=True)
+    print(f"[case] {name} T={tile} {mode} rel_l2={err:.3e} rel_max={rel_max(got, ref):.3e}", flush=True)
     assert err <= GATE
 
 
 EDGE = [
     # (n, cin, h, w, cout, k), tile
+    ((1, 3, 19, 17, 4, 5), 4),     # overlap-add with T = K - 1 (no core)
     ((1, 2, 5, 5, 3, 3), 6),       # image smaller than a tile
     ((1, 2, 6, 6, 3, 3), 6),       # image equal to a tile
     ((2, 3, 13, 29, 4, 3), 6),     # ragged, H != W, n > 1
@@ -76,13 +78,16 @@ EDGE = [
 ]
 
 
+@pytest.mark.parametrize("mode", ["os", "oaa"])
 @pytest.mark.parametrize("shape,tile", EDGE)
 @pytest.mark.parametrize("bias,relu", [(False, False), (True, True)])
-def test_edge_shapes(shape, tile, bias, relu):
+def test_edge_shapes(shape, tile, bias, relu, mode):
     n, cin, h, w, cout, k = shape
+    if mode == "oaa" and tile < k - 1:
+        pytest.skip("overlap-add needs T >= K - 1")
     x, wt = small_layer(n, cin, h, w, cout, k, seed=31)
     b = make_random_bias(cout, cin, k, seed=32) if bias else None
-    _, y = run_layer(x, wt, b, tile, relu=relu)
+    _, y = run_layer(x, wt, b, tile, mode=mode, relu=relu)
     ref = oracle.direct_xcorr2d(x, wt, b, relu=relu)
     assert rel_l2(y, ref) <= GATE
     assert rel_max(y, ref) <= 1e-5
@@ -168,3 +173,21 @@ def test_timing_events_bracket_the_kernels():
     assert rel_l2(y.cpu().numpy(), oracle.direct_xcorr2d(x, w)) <= GATE
     with pytest.raises(ValueError):
         fs.set_timing_events(torch.cuda.Event(enable_timing=True), None)
+
+
+@pytest.mark.parametrize("tile", [6, 14, 30])
+def test_overlap_save_equals_overlap_add(tile):
+    x, w = small_layer(2, 12, 45, 38, 20, 3, seed=71)
+    b = make_random_bias(20, 12, 3, seed=72)
+    _, y_os = run_layer(x, w, b, tile, mode="os", relu=True)
+    _, y_oaa = run_layer(x, w, b, tile, mode="oaa", relu=True)
+    assert rel_l2(y_oaa, y_os) <= 1e-6
+
+
+def test_overlap_add_is_deterministic():
+    x, w = small_layer(1, 8, 40, 40, 16, 5, seed=73)
+    plan = fs.Plan(1, 8, 40, 40, 16, 5, tile=12, mode="oaa")
+    wspec = plan.transform_weights(_dev(w))
+    xd = _dev(x)
+    outs = [plan.conv2d(xd, wspec).cpu().numpy() for _ in range(3)]
+    assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])

@@ -98,12 +98,13 @@ def test_contraction(name, shape, tile):
     assert rel_max(Y, ref) < 1e-5
 
 
+@pytest.mark.parametrize("mode", ["os", "oaa"])
 @pytest.mark.parametrize("relu", [False, True])
 @pytest.mark.parametrize("name,shape,tile", CASES)
-def test_inverse_placement(name, shape, tile, relu):
+def test_inverse_placement(name, shape, tile, relu, mode):
     n, cin, h, w, cout, k = shape
     x, wt = small_layer(n, cin, h, w, cout, k, seed=6)
-    plan = fs.Plan(n, cin, h, w, cout, k, tile=tile, bias=True, relu=relu)
+    plan = fs.Plan(n, cin, h, w, cout, k, tile=tile, bias=True, relu=relu, mode=mode)
     L = plan.nfft
     b = make_random_bias(cout, cin, k, seed=7)
     ws = plan.new_workspace()
@@ -119,7 +120,7 @@ def test_inverse_placement(name, shape, tile, relu):
     full = full.transpose(1, 0, 2, 3).reshape(n, th, tw, cout, L, L)
     # The stored output spectra carry the 1/L^2 of the inverse already; the
     # oracle's inverse divides by L^2 itself.
-    ref = oracle.inverse_place(full * (L * L), h, w, tile, k, "os", b, relu)
+    ref = oracle.inverse_place(full * (L * L), h, w, tile, k, mode, b, relu)
     got = y.cpu().numpy()
     assert rel_l2(got, ref) < 2e-6
     assert rel_max(got, ref) < 1e-5
