@@ -98,12 +98,48 @@ def load_traffic(kernel, workload_tag):
         return None
 
 
+def bench_vgg16(args):
+    """The 13-layer VGG-16 stack at batch 32 (3x224x224 -> 512x7x7), each
+    layer's tile chosen by its plan; a step is one forward of the stack."""
+    import torch
+    import paper_2003_12621_amd as fs  # noqa: F401
+    from paper_2003_12621_amd.vgg import VGG16Stack
+    from workloads import VGG16_LAYERS, VGG_BATCH, make_vgg16
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    x, layers = make_vgg16(batch=VGG_BATCH, seed=0)
+    stack = VGG16Stack(layers, batch=VGG_BATCH, mode=args.mode)
+    xd = torch.from_numpy(x).to(dev)
+    for _ in range(args.warmup):
+        stack.forward(xd)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        stack.forward(xd)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    flops = 0
+    s = 224
+    for i, (cin, cout, hw) in enumerate(VGG16_LAYERS, start=1):
+        flops += 2 * VGG_BATCH * cout * hw * hw * cin * 9
+    out = {"metric": "effective direct-conv GFLOP/s", "value": round(flops / (ms * 1e-3) / 1e9, 1),
+           "unit": "GFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "f32", "data": "synthetic",
+           "config": {"workload": f"vgg16 conv stack, batch {VGG_BATCH}, 3x224x224, bias+ReLU, 5 max-pools",
+                      "tiles": stack.tiles, "mode": args.mode},
+           "images_per_s": round(VGG_BATCH / (ms * 1e-3), 1)}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default=DEFAULT_CONFIG)
+    ap.add_argument("--config", default=DEFAULT_CONFIG, help="a layer config name, or vgg16")
     ap.add_argument("--tile", type=int, default=None)
     ap.add_argument("--mode", default="os", choices=["os", "oaa"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -121,6 +157,8 @@ def main():
     import paper_2003_12621_amd as fs
     from workloads import CONFIGS, make_config
 
+    if args.config == "vgg16":
+        return bench_vgg16(args)
     cfg = CONFIGS[args.config]
     layer = cfg["layer"]
     tile = args.tile if args.tile is not None else (DEFAULT_TILE if args.config == DEFAULT_CONFIG else cfg["tiles"][-1])

@@ -1,0 +1,78 @@
+"""A VGG-16 convolution stack on the split-FFT convolution.
+
+The paper evaluates the method on the convolution layers of VGG16
+(Section 4).  This driver runs the 13 3x3 'same' convolutions with fused
+bias and ReLU and a 2x2 stride-2 max-pool after layers 2, 4, 7, 10 and 13,
+all through the library's C ABI: each layer has its own plan (tile size
+chosen by the plan unless given) and filter spectra, transformed once at
+construction; one workspace (the largest any layer needs) and two
+activation buffers are shared by all layers.
+"""
+from __future__ import annotations
+
+from typing import List, Optional, Sequence
+
+from . import Plan, maxpool2x2
+
+POOL_AFTER = (2, 4, 7, 10, 13)
+
+
+class VGG16Stack:
+    def __init__(self, layers: Sequence, batch: int, hw: int = 224, tiles: Optional[Sequence[int]] = None,
+                 mode: str = "os", device=None):
+        """`layers`: 13 (w, b) pairs (torch CUDA float32 tensors or arrays);
+        `tiles`: optional per-layer tile sizes (0 or None = plan's choice)."""
+        import torch
+        if len(layers) != 13:
+            raise ValueError("VGG-16 has 13 convolution layers")
+        dev = torch.device("cuda", torch.cuda.current_device() if device is None else int(device))
+        self.device = dev
+        self.batch = batch
+        self.plans: List[Plan] = []
+        self.wspecs = []
+        self.biases = []
+        s = hw
+        shapes = []
+        for i, (w, b) in enumerate(layers, start=1):
+            w = torch.as_tensor(w, dtype=torch.float32, device=dev).contiguous()
+            b = torch.as_tensor(b, dtype=torch.float32, device=dev).contiguous()
+            cout, cin, k, _ = w.shape
+            t = 0 if tiles is None or not tiles[i - 1] else int(tiles[i - 1])
+            plan = Plan(batch, cin, s, s, cout, k, tile=t, mode=mode, bias=True, relu=True, device=dev.index)
+            self.plans.append(plan)
+            self.wspecs.append(plan.transform_weights(w))
+            self.biases.append(b)
+            shapes.append((batch, cout, s, s))
+            if i in POOL_AFTER:
+                s //= 2
+        self.workspace = torch.empty(max(p.info.workspace_bytes for p in self.plans), dtype=torch.uint8,
+                                     device=dev)
+        biggest = max(max(n * c * h * w for n, c, h, w in shapes), batch * 3 * hw * hw)
+        self._buf = [torch.empty(biggest, dtype=torch.float32, device=dev) for _ in range(2)]
+
+    @property
+    def tiles(self):
+        return [p.tile for p in self.plans]
+
+    def forward(self, x, keep=False):
+        """Runs the stack on x [batch, 3, hw, hw].  Returns the final
+        activation [batch, 512, hw/32, hw/32] (a view of an internal buffer),
+        or with keep=True also a list of copies of every layer's post-ReLU
+        output (before pooling)."""
+        cur, other = self._buf
+        a = x
+        outs = []
+        for i, plan in enumerate(self.plans, start=1):
+            shape = (plan.n, plan.cout, plan.h, plan.w)
+            y = other[: plan.n * plan.cout * plan.h * plan.w].view(shape)
+            plan.conv2d(a, self.wspecs[i - 1], self.biases[i - 1], out=y, workspace=self.workspace)
+            if keep:
+                outs.append(y.clone())
+            if i in POOL_AFTER:
+                pooled = cur[: plan.n * plan.cout * (plan.h // 2) * (plan.w // 2)].view(
+                    plan.n, plan.cout, plan.h // 2, plan.w // 2)
+                a = maxpool2x2(y, out=pooled)
+            else:
+                a = y
+                cur, other = other, cur
+        return (a, outs) if keep else a

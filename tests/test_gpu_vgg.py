@@ -1,0 +1,59 @@
+"""The VGG-16 stack (13 convolutions with bias+ReLU, 5 max-pools) on the
+split-FFT convolution at batch 32, each layer's tile chosen by its plan.
+
+The oracle runs two sampled images of the batch (images are independent):
+  * as a chain, float64 from the input -- the gate rel-L2 <= 1e-4 on every
+    layer's output and on the final activation;
+  * per layer, fed the GPU's own previous activation -- localises drift to a
+    layer (each layer alone within 1e-5).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from workloads import make_vgg16
+
+from spectra_layout import rel_l2
+
+torch = pytest.importorskip("torch")
+fs = pytest.importorskip("paper_2003_12621_amd")
+
+pytestmark = pytest.mark.gpu
+
+SAMPLE = [0, 1]
+
+
+@pytest.fixture(scope="module")
+def vgg_run():
+    from paper_2003_12621_amd.vgg import VGG16Stack, POOL_AFTER
+    x, layers = make_vgg16(batch=32, seed=0)
+    stack = VGG16Stack(layers, batch=32)
+    out, outs = stack.forward(torch.from_numpy(x).cuda(), keep=True)
+    torch.cuda.synchronize()
+    print(f"[vgg] tiles per layer: {stack.tiles}", flush=True)
+    got = [o[SAMPLE].cpu().numpy() for o in outs]
+    final = out[SAMPLE].cpu().numpy()
+    return x, layers, got, final, POOL_AFTER
+
+
+def test_vgg16_chain_matches_oracle(vgg_run):
+    x, layers, got, final, _ = vgg_run
+    ref_outs, ref_final = oracle.vgg16_forward(x[SAMPLE], layers, return_all=True)
+    assert final.shape == (2, 512, 7, 7)
+    for i, (g, r) in enumerate(zip(got, ref_outs), start=1):
+        err = rel_l2(g, r)
+        print(f"[vgg] layer {i:2d} chain rel_l2 = {err:.3e}", flush=True)
+        assert err <= 1e-4, i
+    assert rel_l2(final, ref_final) <= 1e-4
+
+
+def test_vgg16_each_layer_on_gpu_input(vgg_run):
+    x, layers, got, _, pool_after = vgg_run
+    a = x[SAMPLE].astype(np.float64)
+    for i, (w, b) in enumerate(layers, start=1):
+        ref = oracle.direct_xcorr2d(a, w, b, relu=True)
+        err = rel_l2(got[i - 1], ref)
+        assert err <= 1e-5, (i, err)
+        a = got[i - 1].astype(np.float64)
+        if i in pool_after:
+            a = oracle.maxpool2x2(a)
