@@ -257,11 +257,17 @@ def main():
         "config": {"workload": f"{args.config}: n={layer.n} cin={layer.cin} {layer.h}x{layer.w} "
                                f"cout={layer.cout} k={layer.k} stride1 same",
                    "tile": info.tile, "nfft": info.nfft, "mode": args.mode, "tiles": info.tiles,
-                   "bins": info.bins},
+                   "bins": info.bins,
+                   "contract_variant": f"{info.contract_tile_m}x{info.contract_tile_n}x{info.contract_stage_k}"
+                                       f"/{info.contract_real_products}M"},
         "images_per_s": round(layer.n / (ms_per_step * 1e-3), 1),
         "roofline": {"bound": "mfma", "kernel": "contract (per-bin complex Cin->Cout product)",
                      "achieved": round(con_tfs, 2), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(con_tfs / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": traffic},
+                     "frac": round(con_tfs / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": traffic,
+                     "flops_per_complex_mac": 8,
+                     "mfma_real_products_per_complex_mac": info.contract_real_products,
+                     "mfma_executed_frac": round(con_tfs * info.contract_real_products / 4
+                                                 / FP32_MFMA_PEAK_TFLOPS, 4)},
         "stages": {
             "forward": {"ms": round(avg(fwd), 4), "GB/s": round(fwd_gbs, 1),
                         "frac_hbm": round(fwd_gbs / HBM_PEAK_GBS, 4), "bytes": counts["forward_bytes"],

@@ -113,6 +113,12 @@ typedef struct {
     size_t xspec_offset, xspec_bytes;
     size_t yspec_offset, yspec_bytes;
     size_t aux_offset, aux_bytes;   /* overlap-add seam partials (0 for overlap-save) */
+    /* Contraction kernel variant chosen by the plan: output tile
+     * contract_tile_m channels x contract_tile_n patches, input channels in
+     * stages of contract_stage_k, and 3 (Gauss) or 4 real matrix products
+     * per complex multiply-add.  The environment variable
+     * FFTSPLIT_CONTRACT_TILE=[g3:|g4:]MxNxK overrides it at plan time. */
+    int contract_tile_m, contract_tile_n, contract_stage_k, contract_real_products;
 } fftsplit_plan_info_t;
 
 /* Validate `prob` (host) and create a plan for `device` (a HIP ordinal).

@@ -46,7 +46,9 @@ class PlanInfo(ctypes.Structure):
                 ("wspec_bytes", ctypes.c_size_t), ("workspace_bytes", ctypes.c_size_t),
                 ("xspec_offset", ctypes.c_size_t), ("xspec_bytes", ctypes.c_size_t),
                 ("yspec_offset", ctypes.c_size_t), ("yspec_bytes", ctypes.c_size_t),
-                ("aux_offset", ctypes.c_size_t), ("aux_bytes", ctypes.c_size_t)]
+                ("aux_offset", ctypes.c_size_t), ("aux_bytes", ctypes.c_size_t),
+                ("contract_tile_m", ctypes.c_int), ("contract_tile_n", ctypes.c_int),
+                ("contract_stage_k", ctypes.c_int), ("contract_real_products", ctypes.c_int)]
 
 
 class FftsplitError(RuntimeError):

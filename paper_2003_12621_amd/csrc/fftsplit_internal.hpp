@@ -21,6 +21,9 @@ struct fftsplit_plan_s {
     size_t wspec_bytes;
     size_t xspec_off, xspec_bytes, yspec_off, yspec_bytes, aux_off, aux_bytes;
     size_t ws_bytes;
+    // contraction kernel variant: tile BM x BN, KC channels per stage, and
+    // 3 (Gauss) or 4 real products per complex multiply-add
+    int con_bm, con_bn, con_kc, con_products;
 };
 
 namespace fftsplit {

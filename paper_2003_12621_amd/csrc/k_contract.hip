@@ -13,6 +13,11 @@
 // so every operand fragment is 32 consecutive complex values of one input
 // channel row, and every stored output row is 32 consecutive patches.
 //
+// With G3 the complex product takes three real products instead (Gauss):
+//     P1 = Wr Xr, P2 = Wi Xi, P3 = (Wr + Wi)(Xr + Xi);  Y = (P1 - P2, P3 - P1 - P2)
+// which cuts the matrix-core work by a quarter for two vector adds per
+// operand fragment; the plan's default.
+//
 // Workgroup tile: BM output channels x BN patches of one bin, 4 waves in a
 // WM x (4/WM) grid.  The input-channel loop runs in stages of KC channels;
 // stage s+1 is loaded from memory into registers while stage s is
@@ -21,9 +26,6 @@
 // pair are read from LDS while the current pair's MFMAs run.  The channel
 // blocks of one bin are consecutive logical workgroups on the same XCD, so
 // the bin's patch spectra are fetched from HBM once and reused from L2.
-#include <cstdlib>
-#include <cstring>
-
 #include "fftsplit_internal.hpp"
 #include "launch_util.hpp"
 
@@ -47,7 +49,7 @@ struct ConShape {
     static_assert((WE / 2) % NT == 0 && (XE / 2) % NT == 0, "loads divide evenly");
 };
 
-template <int BM, int BN, int KC, int WM>
+template <int BM, int BN, int KC, int WM, bool G3>
 __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict__ xs, const float2* __restrict__ ws,
                                                        float2* __restrict__ ys, int cin, int coutp, int ntp,
                                                        int nbco, int nbt) {
@@ -119,7 +121,10 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
         for (int i = 0; i < S::XL; ++i) sx[i * S::NT + tid] = xreg[i];
     };
 
-    floatx16 accR[TM][TN], accI[TM][TN];
+    // 4M: accR = sum Wr Xr - Wi Xi, accI = sum Wr Xi + Wi Xr.
+    // 3M: accR = sum Wr Xr, accI = sum Wi Xi, acc3 = sum (Wr + Wi)(Xr + Xi);
+    //     Y = (accR - accI, acc3 - accR - accI).
+    floatx16 accR[TM][TN], accI[TM][TN], acc3[G3 ? TM : 1][G3 ? TN : 1];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -128,6 +133,7 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
             for (int r = 0; r < 16; ++r) {
                 accR[i][j][r] = 0.f;
                 accI[i][j][r] = 0.f;
+                if (G3) acc3[G3 ? i : 0][G3 ? j : 0][r] = 0.f;
             }
 
     const int nstage = (cin + KC - 1) / KC;
@@ -156,18 +162,35 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
 #pragma unroll
                 for (int j = 0; j < TN; ++j) b[cur ^ 1][j] = sx[(2 * kp + 2) * BN + j * 32];
             }
+            if (G3) {
+                float bs_[TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i) {
-                const float ar = a[cur][i].x, ai = a[cur][i].y, nai = -ai;
+                for (int j = 0; j < TN; ++j) bs_[j] = b[cur][j].x + b[cur][j].y;
 #pragma unroll
-                for (int j = 0; j < TN; ++j) {
-                    accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ar, b[cur][j].x, accR[i][j], 0, 0, 0);
-                    accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ar, b[cur][j].y, accI[i][j], 0, 0, 0);
+                for (int i = 0; i < TM; ++i) {
+                    const float ar = a[cur][i].x, ai = a[cur][i].y, as_ = ar + ai;
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) {
+                        accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ar, b[cur][j].x, accR[i][j], 0, 0, 0);
+                        accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ai, b[cur][j].y, accI[i][j], 0, 0, 0);
+                        acc3[G3 ? i : 0][G3 ? j : 0] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                            as_, bs_[j], acc3[G3 ? i : 0][G3 ? j : 0], 0, 0, 0);
+                    }
                 }
+            } else {
 #pragma unroll
-                for (int j = 0; j < TN; ++j) {
-                    accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(nai, b[cur][j].y, accR[i][j], 0, 0, 0);
-                    accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ai, b[cur][j].x, accI[i][j], 0, 0, 0);
+                for (int i = 0; i < TM; ++i) {
+                    const float ar = a[cur][i].x, ai = a[cur][i].y, nai = -ai;
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) {
+                        accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ar, b[cur][j].x, accR[i][j], 0, 0, 0);
+                        accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ar, b[cur][j].y, accI[i][j], 0, 0, 0);
+                    }
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) {
+                        accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(nai, b[cur][j].y, accR[i][j], 0, 0, 0);
+                        accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ai, b[cur][j].x, accI[i][j], 0, 0, 0);
+                    }
                 }
             }
         }
@@ -184,17 +207,22 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int ii = 8 * (r >> 2) + 4 * krow + (r & 3);
-                yb[size_t(ii) * ntp] = make_float2(accR[i][j][r], accI[i][j][r]);
+                if (G3) {
+                    const float p1 = accR[i][j][r], p2 = accI[i][j][r];
+                    yb[size_t(ii) * ntp] = make_float2(p1 - p2, acc3[G3 ? i : 0][G3 ? j : 0][r] - p1 - p2);
+                } else {
+                    yb[size_t(ii) * ntp] = make_float2(accR[i][j][r], accI[i][j][r]);
+                }
             }
         }
     }
 }
 
-template <int BM, int BN, int KC, int WM>
+template <int BM, int BN, int KC, int WM, bool G3 = false>
 static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, const float2* ws, float2* ys,
                                     hipStream_t s, const LaunchEvents& ev) {
     using S = ConShape<BM, BN, KC, WM>;
-    auto kern = contract_kernel<BM, BN, KC, WM>;
+    auto kern = contract_kernel<BM, BN, KC, WM, G3>;
     static hipError_t attr = allow_dynamic_lds(kern, S::LDS_BYTES);
     if (attr != hipSuccess) return attr;
     if (p.coutp % BM != 0 || p.ntp % BN != 0) return hipErrorInvalidValue;
@@ -204,28 +232,27 @@ static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, 
                          p.prob.cin, p.coutp, p.ntp, nbco, nbt);
 }
 
-// Tile variants, by name "BMxBNxKC" (wave grid fixed per shape).
-hipError_t launch_contract_variant(const char* v, const fftsplit_plan_s& p, const float2* xs, const float2* ws,
-                                   float2* ys, hipStream_t s, const LaunchEvents& ev) {
-    if (!std::strcmp(v, "64x64x16")) return launch_contract_v<64, 64, 16, 2>(p, xs, ws, ys, s, ev);
-    if (!std::strcmp(v, "64x64x32")) return launch_contract_v<64, 64, 32, 2>(p, xs, ws, ys, s, ev);
-    if (!std::strcmp(v, "128x64x16")) return launch_contract_v<128, 64, 16, 2>(p, xs, ws, ys, s, ev);
-    if (!std::strcmp(v, "128x64x32")) return launch_contract_v<128, 64, 32, 2>(p, xs, ws, ys, s, ev);
-    if (!std::strcmp(v, "64x128x16")) return launch_contract_v<64, 128, 16, 2>(p, xs, ws, ys, s, ev);
-    if (!std::strcmp(v, "128x128x16")) return launch_contract_v<128, 128, 16, 2>(p, xs, ws, ys, s, ev);
-    if (!std::strcmp(v, "256x64x16")) return launch_contract_v<256, 64, 16, 4>(p, xs, ws, ys, s, ev);
-    return hipErrorInvalidValue;
-}
-
 hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xs, const float2* ws, float2* ys,
                            hipStream_t s, const LaunchEvents& ev) {
-    // FFTSPLIT_CONTRACT_TILE=BMxBNxKC selects a tile variant (tuning aid).
-    if (const char* v = std::getenv("FFTSPLIT_CONTRACT_TILE")) {
-        if (*v) return launch_contract_variant(v, p, xs, ws, ys, s, ev);
+    const int v = p.con_bm * 1000000 + p.con_bn * 1000 + p.con_kc;
+    if (p.con_products == 3) {
+        switch (v) {
+            case 64064016: return launch_contract_v<64, 64, 16, 2, true>(p, xs, ws, ys, s, ev);
+            case 128064016: return launch_contract_v<128, 64, 16, 2, true>(p, xs, ws, ys, s, ev);
+            case 64128016: return launch_contract_v<64, 128, 16, 2, true>(p, xs, ws, ys, s, ev);
+        }
+    } else {
+        switch (v) {
+            case 64064016: return launch_contract_v<64, 64, 16, 2>(p, xs, ws, ys, s, ev);
+            case 64064032: return launch_contract_v<64, 64, 32, 2>(p, xs, ws, ys, s, ev);
+            case 128064016: return launch_contract_v<128, 64, 16, 2>(p, xs, ws, ys, s, ev);
+            case 128064032: return launch_contract_v<128, 64, 32, 2>(p, xs, ws, ys, s, ev);
+            case 64128016: return launch_contract_v<64, 128, 16, 2>(p, xs, ws, ys, s, ev);
+            case 128128016: return launch_contract_v<128, 128, 16, 2>(p, xs, ws, ys, s, ev);
+            case 256064016: return launch_contract_v<256, 64, 16, 4>(p, xs, ws, ys, s, ev);
+        }
     }
-    // 64x64 tiles with 16-channel stages measured fastest on every layer
-    // shape tried (small register and LDS footprint: 7 waves per SIMD).
-    return launch_contract_v<64, 64, 16, 2>(p, xs, ws, ys, s, ev);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace fftsplit

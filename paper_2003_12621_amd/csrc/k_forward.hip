@@ -62,38 +62,46 @@ __global__ __launch_bounds__(TG * (L / 2)) void forward_kernel(const float* __re
     // 1. gather.  Wave wv reads the windows of its own TPW patches; each
     // wave-wide load covers RPI consecutive window rows of one patch (L
     // consecutive lanes per row), so the patch geometry is wave-uniform.
+    // Each patch gets a buffer descriptor whose range ends where its valid
+    // rows end; rows before it wrap to huge offsets, and lanes whose column
+    // is outside the image (or, for overlap-add, beyond the tile) use an
+    // always-out-of-range offset -- all of those read 0.
     {
         const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
         const int lane = tid & 63;
         const int q = lane % L;
         const int mr = lane / L;
+        const unsigned row_step = unsigned(RPI * w * 4);
         float v[S::NLOAD];
 #pragma unroll
         for (int pi = 0; pi < TPW; ++pi) {
-            const int u = wv * TPW + pi;
-            const int t = t0 + u;
-            int r0 = -(1 << 29), c0 = 0, base = 0;   // padding patches read nothing
+            const int t = t0 + wv * TPW + pi;
+            const float* base = x;
+            unsigned bytes = 0, voff = kOutOfRange;   // padding patches read nothing
             if (t < nt) {
                 const int b = t % tw;
                 const int rest = t / tw;
                 const int a = rest % th;
                 const int img = rest / th;
-                r0 = OAA ? a * T : a * T - P;
-                c0 = OAA ? b * T : b * T - P;
-                base = (img * cin + c) * h * w;
+                const int plane = (img * cin + c) * h * w;
+                if (OAA) {
+                    // rows a*T .. min(a*T + T, h) - 1 of the plane, cols b*T + q for q < T
+                    base = x + plane + a * T * w;
+                    bytes = unsigned(min(T, h - a * T) * w * 4);
+                    const int col = b * T + q;
+                    if (q < T && col < w) voff = unsigned((mr * w + col) * 4);
+                } else {
+                    // rows a*T - P + m of the plane; rows < 0 wrap out of range
+                    base = x + plane;
+                    bytes = unsigned(h * w * 4);
+                    const int col = b * T - P + q;
+                    if (unsigned(col) < unsigned(w)) voff = unsigned(((a * T - P + mr) * w + col) * 4);
+                }
             }
+            const BufRsrc rs = make_rsrc(base, bytes);
 #pragma unroll
-            for (int ri = 0; ri < L / RPI; ++ri) {
-                const int m = ri * RPI + mr;
-                int r = r0 + m;
-                int col = c0 + q;
-                bool ok = unsigned(r) < unsigned(h) && unsigned(col) < unsigned(w);
-                if (OAA) ok = ok && m < T && q < T;
-                r = min(max(r, 0), h - 1);
-                col = min(max(col, 0), w - 1);
-                const float val = x[base + r * w + col];
-                v[pi * (L / RPI) + ri] = ok ? val : 0.f;
-            }
+            for (int ri = 0; ri < L / RPI; ++ri)
+                v[pi * (L / RPI) + ri] = buf_load_f32(rs, voff + unsigned(ri) * row_step, 0);
         }
 #pragma unroll
         for (int pi = 0; pi < TPW; ++pi) {
@@ -139,20 +147,23 @@ __global__ __launch_bounds__(TG * (L / 2)) void forward_kernel(const float* __re
             for (int m = 0; m < L; ++m) cz[m] = cb[m * TP + j];
         }
         fft<L, false>(cz);
-        const size_t bs = size_t(cin) * ntp;
-        float2* out = xs + size_t(c) * ntp + t0 + u;
+        // X[f][c][t0 + u]: per-lane byte offset, per-bin stride as the
+        // scalar offset (always in range).
+        const BufRsrc rx = make_rsrc(xs, unsigned(size_t(cin) * ntp * 8 * stored_bins(L)));
+        const unsigned bs8 = unsigned(cin) * unsigned(ntp) * 8u;
+        const unsigned voff = unsigned(c * ntp + t0 + u) * 8u;
         if (j == 0) {
 #pragma unroll
             for (int k1 = 0; k1 <= H2; ++k1) {
                 float2 a, b;
                 split_two_real(cz[k1], cz[(L - k1) % L], a, b);
-                out[size_t(bin_col0(L, k1)) * bs] = a;
-                out[size_t(bin_colh(L, k1)) * bs] = b;
+                buf_store_f32x2(a, rx, voff, unsigned(bin_col0(L, k1)) * bs8);
+                buf_store_f32x2(b, rx, voff, unsigned(bin_colh(L, k1)) * bs8);
             }
         } else {
-            float2* o = out + size_t(bin_mid(L, 0, j)) * bs;
+            const unsigned vj = voff + unsigned(bin_mid(L, 0, j)) * bs8;
 #pragma unroll
-            for (int k1 = 0; k1 < L; ++k1) o[size_t(k1) * bs] = cz[k1];
+            for (int k1 = 0; k1 < L; ++k1) buf_store_f32x2(cz[k1], rx, vj, unsigned(k1) * bs8);
         }
     }
 }

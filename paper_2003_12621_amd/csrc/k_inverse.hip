@@ -53,7 +53,7 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
                                                                const float* __restrict__ bias, float* __restrict__ y,
                                                                float* __restrict__ aux, int cout, int coutp, int h,
                                                                int w, int T, int P, int th, int tw, int nt, int ntp,
-                                                               int ngroups, int relu) {
+                                                               int ngroups, int relu, int y_elems) {
     using S = InvShape<L, TG>;
     constexpr int H2 = S::H2, NT = S::NT, TP = S::TP, TTS = S::TTS, SP = S::SP, STS = S::STS;
     extern __shared__ float4 lds_raw[];
@@ -87,19 +87,21 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
         cols_ok[tid] = cw;
     }
 
-    // 1. column pass
+    // 1. column pass: Y[f][co][t0 + u] with a per-lane byte offset and the
+    // per-bin stride as the scalar offset (always in range).
     {
         const int u = tid % TG;
         const int j = tid / TG;
-        const size_t bs = size_t(coutp) * ntp;
-        const float2* in = ys + size_t(co) * ntp + t0 + u;
+        const BufRsrc ry = make_rsrc(ys, unsigned(size_t(coutp) * ntp * 8 * stored_bins(L)));
+        const unsigned bs8 = unsigned(coutp) * unsigned(ntp) * 8u;
+        const unsigned voff = unsigned(co * ntp + t0 + u) * 8u;
         float2 cz[L];
         if (j == 0) {
             float2 y0[H2 + 1], yh[H2 + 1];
 #pragma unroll
             for (int k1 = 0; k1 <= H2; ++k1) {
-                y0[k1] = in[size_t(bin_col0(L, k1)) * bs];
-                yh[k1] = in[size_t(bin_colh(L, k1)) * bs];
+                y0[k1] = buf_load_f32x2(ry, voff, unsigned(bin_col0(L, k1)) * bs8);
+                yh[k1] = buf_load_f32x2(ry, voff, unsigned(bin_colh(L, k1)) * bs8);
             }
 #pragma unroll
             for (int k1 = 0; k1 < L; ++k1) {
@@ -111,9 +113,9 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
                 }
             }
         } else {
-            const float2* src = in + size_t(bin_mid(L, 0, j)) * bs;
+            const unsigned vj = voff + unsigned(bin_mid(L, 0, j)) * bs8;
 #pragma unroll
-            for (int k1 = 0; k1 < L; ++k1) cz[k1] = src[size_t(k1) * bs];
+            for (int k1 = 0; k1 < L; ++k1) cz[k1] = buf_load_f32x2(ry, vj, unsigned(k1) * bs8);
         }
         fft<L, true>(cz);
         float2* cb = tb + u * TTS;
@@ -165,6 +167,7 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
         const int ms = tid / (L * S::US);
         const float bv = bias ? bias[co] : 0.f;
         const int cs = T - 2 * P;  // overlap-add core size
+        const BufRsrc ry_out = make_rsrc(y, unsigned(size_t(y_elems) * 4));
 #pragma unroll 4
         for (int ub = 0; ub < TG; ub += S::US) {
             const int u = ub + us;
@@ -172,14 +175,17 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
             const int d = dst_off[u];
             const float* s = st + u * STS;
             if (!OAA) {
+                // Output through a descriptor over y: lanes outside the crop
+                // (m >= ro or q >= cw) get an out-of-range offset, which drops
+                // the store.
+                const unsigned vq = unsigned(d + q) * 4u;
 #pragma unroll
                 for (int mb = 0; mb < L; mb += S::MS) {
                     const int m = mb + ms;
-                    if (m < ro && q < cw) {
-                        float v = s[m * SP + q] + bv;
-                        if (relu) v = fmaxf(v, 0.f);
-                        y[d + m * w + q] = v;
-                    }
+                    float v = s[m * SP + q] + bv;
+                    if (relu) v = fmaxf(v, 0.f);
+                    const unsigned vo = (m < ro && q < cw) ? vq + unsigned(m * w) * 4u : kOutOfRange;
+                    buf_store_f32(v, ry_out, vo, 0);
                 }
             } else if (t0 + u < nt) {
                 float* slot = aux + (co * ntp + t0 + u) * (L * L);
@@ -251,7 +257,7 @@ static hipError_t launch_inverse_v(const fftsplit_plan_s& p, const float2* ys, c
     const dim3 grid(unsigned(ngroups) * unsigned(p.prob.cout));
     hipError_t e = launch_kernel(kern, grid, dim3(S::NT), S::LDS_BYTES, s, ev.start, OAA ? nullptr : ev.stop, ys,
                                  bias, y, aux, p.prob.cout, p.coutp, p.prob.h, p.prob.w, p.T, p.P, p.th, p.tw, p.nt,
-                                 p.ntp, ngroups, int(p.relu));
+                                 p.ntp, ngroups, int(p.relu), p.prob.n * p.prob.cout * p.prob.h * p.prob.w);
     if (e != hipSuccess || !OAA) return e;
     const dim3 sgrid(unsigned((p.prob.h * p.prob.w + 255) / 256), unsigned(p.prob.n * p.prob.cout));
     return launch_kernel(seam_kernel, sgrid, dim3(256), 0, s, nullptr, ev.stop, aux, bias, y, p.prob.cout, p.prob.h,

@@ -29,6 +29,31 @@ inline hipError_t allow_dynamic_lds(K kernel, int bytes) {
                                bytes);
 }
 
+// Raw buffer access (gfx9 buffer descriptors).  A load whose byte offset
+// (VGPR offset; the scalar offset is only used for accesses known to be in
+// range) is at or beyond `bytes` returns 0 and a store there is dropped, so
+// padding outside an image costs no compare-and-select per element.
+typedef __amdgpu_buffer_rsrc_t BufRsrc;
+constexpr unsigned kOutOfRange = 0x80000000u;   // offset that is always out of range
+
+__device__ __forceinline__ BufRsrc make_rsrc(const void* base, unsigned bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ float buf_load_f32(BufRsrc r, unsigned voff, unsigned soff) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+__device__ __forceinline__ float2 buf_load_f32x2(BufRsrc r, unsigned voff, unsigned soff) {
+    typedef int int2v __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+}
+__device__ __forceinline__ void buf_store_f32(float v, BufRsrc r, unsigned voff, unsigned soff) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, voff, soff, 0);
+}
+__device__ __forceinline__ void buf_store_f32x2(float2 v, BufRsrc r, unsigned voff, unsigned soff) {
+    typedef int int2v __attribute__((ext_vector_type(2)));
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(int2v, v), r, voff, soff, 0);
+}
+
 // Optional timing events of one entry-point call: `start` is recorded when
 // the call's first kernel begins and `stop` when its last kernel ends
 // (hipExtLaunchKernel timestamps, no separate event packets).

@@ -7,6 +7,7 @@
 // the L whose modelled time (streamed bytes at an effective bandwidth plus
 // contraction flops at an effective matrix-core rate) is smallest.
 #include <cerrno>
+#include <cstdint>
 #include <climits>
 #include <cstdio>
 #include <cstdlib>
@@ -143,8 +144,11 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     if (!mul_ok(size_t(p.n) * size_t(p.h), size_t(p.w), &tmp) ||
         !mul_ok(tmp, size_t(p.cin > p.cout ? p.cin : p.cout), &img_elems))
         return fail(FFTSPLIT_ERROR_INVALID_VALUE, "tensor sizes overflow size_t");
-    if (img_elems > size_t(INT_MAX))
-        return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "input/output tensors above 2^31 elements are not supported");
+    // ... and with 32-bit byte offsets inside buffer descriptors.
+    if (img_elems > size_t(INT_MAX) / 4)
+        return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "input/output tensors above 2^29 elements are not supported");
+    if (xs > size_t(UINT32_MAX) || ys > size_t(UINT32_MAX))
+        return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "patch/output spectra above 4 GiB are not supported");
 
     // Architecture check.
     char archbuf[64] = {0};
@@ -187,6 +191,37 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     // Overlap-add keeps each patch's L x L inverse result for the seam pass.
     plan->aux_bytes = oaa ? size_t(p.cout) * size_t(g.ntp) * size_t(g.L) * size_t(g.L) * 4 : 0;
     plan->ws_bytes = plan->aux_off + plan->aux_bytes;
+
+    // Contraction variant: 64x64 tiles, 16-channel stages, three real
+    // products per complex multiply-add (fastest measured on every layer
+    // shape); FFTSPLIT_CONTRACT_TILE=[g3:|g4:]BMxBNxKC overrides.
+    plan->con_bm = 64;
+    plan->con_bn = 64;
+    plan->con_kc = 16;
+    plan->con_products = 3;
+    if (const char* v = std::getenv("FFTSPLIT_CONTRACT_TILE")) {
+        if (*v) {
+            int prod = 4;
+            const char* q = v;
+            if (!std::strncmp(q, "g3:", 3)) { prod = 3; q += 3; }
+            else if (!std::strncmp(q, "g4:", 3)) { q += 3; }
+            int bm = 0, bn = 0, kc = 0;
+            if (std::sscanf(q, "%dx%dx%d", &bm, &bn, &kc) != 3) {
+                delete plan;
+                return fail(FFTSPLIT_ERROR_INVALID_VALUE, "FFTSPLIT_CONTRACT_TILE must look like [g3:]BMxBNxKC");
+            }
+            plan->con_bm = bm;
+            plan->con_bn = bn;
+            plan->con_kc = kc;
+            plan->con_products = prod;
+        }
+    }
+    if (g.coutp % plan->con_bm != 0 || g.ntp % plan->con_bn != 0) {
+        const int bm = plan->con_bm, bn = plan->con_bn;
+        delete plan;
+        return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "contraction tile " + std::to_string(bm) + "x" + std::to_string(bn) +
+                                                      " does not divide the padded problem");
+    }
 
     const char* log = std::getenv("FFTSPLIT_LOG");
     if (log && *log && *log != '0') {
@@ -238,6 +273,10 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_plan_info(fftsplit_plan_t plan, fftsp
     i.yspec_bytes = plan->yspec_bytes;
     i.aux_offset = plan->aux_off;
     i.aux_bytes = plan->aux_bytes;
+    i.contract_tile_m = plan->con_bm;
+    i.contract_tile_n = plan->con_bn;
+    i.contract_stage_k = plan->con_kc;
+    i.contract_real_products = plan->con_products;
     *out = i;
     return FFTSPLIT_SUCCESS;
 }
