@@ -13,6 +13,7 @@
 struct fftsplit_plan_s {
     fftsplit_problem_t prob;
     int device;                 // HIP ordinal, or -1 for an architecture-only plan
+    int cus;                    // compute units of the device (256 for an architecture-only plan)
     char arch[64];
     int T, L, P;                // tile, FFT size, K/2
     int th, tw, nt, ntp;        // tile grid, tiles, padded tiles
@@ -24,6 +25,11 @@ struct fftsplit_plan_s {
     // contraction kernel variant: tile BM x BN, KC channels per stage, and
     // 3 (Gauss) or 4 real products per complex multiply-add
     int con_bm, con_bn, con_kc, con_products;
+    // overlap-save band variant of the forward transform (band.hpp):
+    // used if fwd_band; LDS row pitch, left zero columns, zero-row slot and
+    // dynamic LDS bytes
+    bool fwd_band;
+    int fwd_bp, fwd_co, fwd_zslot, fwd_lds;
 };
 
 namespace fftsplit {
@@ -31,6 +37,20 @@ namespace fftsplit {
 // Granularity of the contraction's output tiles (patches x channels).
 constexpr int kTileGranule = 64;
 constexpr int kCoutGranule = 64;
+
+// Patches per work item of the forward/inverse transforms (L/2 threads
+// each), by FFT size.
+__host__ __device__ constexpr int patch_group(int L) { return L == 8 ? 64 : (L == 16 ? 32 : 16); }
+
+// Patch stride (float2) of the half spectra in the band variant of the
+// forward transform: L rows of L/2+1 bins, plus one to make it odd.
+__host__ __device__ constexpr int band_half_stride(int L) { return L * (L / 2 + 1) + 1; }
+
+// Band loads per thread (16 bytes each) the band variant of the forward
+// transform holds in registers, by FFT size.
+constexpr int kBandNV8 = 8;
+constexpr int kBandNV16 = 8;
+constexpr int kBandNV32 = 16;
 
 // Number of stored frequency bins of an L x L real transform.
 __host__ __device__ constexpr int stored_bins(int L) { return L * L / 2 + 2; }

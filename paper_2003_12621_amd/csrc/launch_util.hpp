@@ -29,6 +29,27 @@ inline hipError_t allow_dynamic_lds(K kernel, int bytes) {
                                bytes);
 }
 
+// Workgroups of `kernel` (with `threads` threads and `lds` bytes of dynamic
+// LDS) that one compute unit holds at once; at least 1.
+template <typename K>
+inline int resident_blocks(K kernel, int threads, int lds) {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(kernel), threads, lds) !=
+            hipSuccess ||
+        n < 1)
+        n = 1;
+    return n;
+}
+
+// Items per workgroup for a kernel that walks consecutive work items:
+// enough that the grid fits the `slots` workgroups the device holds at once
+// (a single wave of workgroups), at least 1.
+inline int items_per_workgroup(int nitems, int slots) {
+    if (slots < 1) slots = 1;
+    const int ipw = (nitems + slots - 1) / slots;
+    return ipw < 1 ? 1 : ipw;
+}
+
 // Raw buffer access (gfx9 buffer descriptors).  A load whose byte offset
 // (VGPR offset; the scalar offset is only used for accesses known to be in
 // range) is at or beyond `bytes` returns 0 and a store there is dropped, so
@@ -46,12 +67,27 @@ __device__ __forceinline__ float2 buf_load_f32x2(BufRsrc r, unsigned voff, unsig
     typedef int int2v __attribute__((ext_vector_type(2)));
     return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
 }
+__device__ __forceinline__ float4 buf_load_f32x4(BufRsrc r, unsigned voff, unsigned soff) {
+    return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ __forceinline__ void buf_store_f32x4(float4 v, BufRsrc r, unsigned voff, unsigned soff) {
+    typedef int int4v __attribute__((ext_vector_type(4)));
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(int4v, v), r, voff, soff, 0);
+}
 __device__ __forceinline__ void buf_store_f32(float v, BufRsrc r, unsigned voff, unsigned soff) {
     __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, voff, soff, 0);
 }
 __device__ __forceinline__ void buf_store_f32x2(float2 v, BufRsrc r, unsigned voff, unsigned soff) {
     typedef int int2v __attribute__((ext_vector_type(2)));
     __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(int2v, v), r, voff, soff, 0);
+}
+
+// Waits until every vector memory operation this wave has issued is done.
+// Placed where a loop's prefetched loads are consumed, so that the
+// stores issued afterwards never make a later wait include them.
+__device__ __forceinline__ void wait_vmem_all() {
+    // s_waitcnt vmcnt(0), expcnt and lgkmcnt left at their no-wait maximum
+    __builtin_amdgcn_s_waitcnt(0x0F70);
 }
 
 // Optional timing events of one entry-point call: `start` is recorded when

@@ -15,6 +15,7 @@
 #include <new>
 #include <string>
 
+#include "band.hpp"
 #include "fftsplit_internal.hpp"
 
 namespace fftsplit {
@@ -71,6 +72,45 @@ static Geometry geometry(const fftsplit_problem_t& p, int L) {
 }
 
 static bool supported_L(int L) { return L == 8 || L == 16 || L == 32; }
+
+// The band variant of the forward transform (overlap-save, image width a
+// multiple of 4 and at most 256) is used when its band of any work item fits
+// the registers it prefetches into and its LDS stays within two workgroups
+// per compute unit.  FFTSPLIT_FORWARD_BAND=0 turns it off.
+static void choose_forward_band(fftsplit_plan_s& p) {
+    p.fwd_band = false;
+    const int w = p.prob.w, L = p.L, T = p.T, P = p.P;
+    // (offsets are 32-bit; the tile and row arithmetic uses exact float
+    // division, valid below 2^22; stores dropped with an out-of-range
+    // offset need spectra below 2 GiB)
+    if (p.oaa || w % 4 != 0 || w > 256 || p.nt >= (1 << 22) || p.prob.h >= (1 << 22) ||
+        p.xspec_bytes >= (size_t(1) << 31))
+        return;
+    if (const char* e = std::getenv("FFTSPLIT_FORWARD_BAND"))
+        if (*e == '0') return;
+    const int tg = patch_group(L);
+    const int nw = tg * (L / 2) / 64;
+    const int rpi = 64 / (w / 4);
+    const int nv = L == 8 ? kBandNV8 : (L == 16 ? kBandNV16 : kBandNV32);
+    int slots = 0;
+    for (int t0 = 0; t0 < p.nt; t0 += tg) {
+        const BandGeom g = band_geom(t0, tg, p.nt, p.prob.h, T, P, p.th, p.tw);
+        if (g.slots > slots) slots = g.slots;
+    }
+    if ((slots + nw * rpi - 1) / (nw * rpi) > nv) return;
+    const int co = P;
+    int bp = co + p.tw * T + P;
+    if (bp % 2 == 0) ++bp;   // odd pitch: a patch's row-pass lanes read distinct banks
+    const size_t band = size_t(slots + 1) * bp * 4;
+    const size_t half = size_t(tg) * band_half_stride(L) * 8;
+    const size_t lds = band > half ? band : half;
+    if (lds > 80 * 1024) return;
+    p.fwd_band = true;
+    p.fwd_bp = bp;
+    p.fwd_co = co;
+    p.fwd_zslot = slots;
+    p.fwd_lds = int(lds);
+}
 
 static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, const char* arch,
                                     fftsplit_plan_t* out) {
@@ -152,12 +192,14 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
 
     // Architecture check.
     char archbuf[64] = {0};
+    int cus = 256;   // MI355X
     if (device >= 0) {
         hipDeviceProp_t prop;
         hipError_t e = hipGetDeviceProperties(&prop, device);
         if (e != hipSuccess)
             return fail(FFTSPLIT_ERROR_DEVICE, std::string("hipGetDeviceProperties: ") + hipGetErrorString(e));
         std::snprintf(archbuf, sizeof(archbuf), "%s", prop.gcnArchName);
+        if (prop.multiProcessorCount > 0) cus = prop.multiProcessorCount;
     } else {
         std::snprintf(archbuf, sizeof(archbuf), "%s", arch ? arch : "");
     }
@@ -169,6 +211,7 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     plan->prob = p;
     plan->prob.tile = g.T;
     plan->device = device;
+    plan->cus = cus;
     std::snprintf(plan->arch, sizeof(plan->arch), "%s", archbuf);
     plan->T = g.T;
     plan->L = g.L;
@@ -222,6 +265,8 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
         return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "contraction tile " + std::to_string(bm) + "x" + std::to_string(bn) +
                                                       " does not divide the padded problem");
     }
+
+    choose_forward_band(*plan);
 
     const char* log = std::getenv("FFTSPLIT_LOG");
     if (log && *log && *log != '0') {
