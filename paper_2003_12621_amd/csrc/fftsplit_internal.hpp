@@ -30,6 +30,10 @@ struct fftsplit_plan_s {
     // dynamic LDS bytes
     bool fwd_band;
     int fwd_bp, fwd_co, fwd_zslot, fwd_lds;
+    // overlap-save band variant of the inverse transform: used if
+    // inv_band; LDS pitch of the output band and dynamic LDS bytes
+    bool inv_band;
+    int inv_obp, inv_lds;
 };
 
 namespace fftsplit {

@@ -25,6 +25,7 @@
 //      the 1-4 contributions of every seam pixel in a fixed order (no
 //      atomics, deterministic) and applies bias and ReLU.
 // The inverse's 1/L^2 is already folded into the filter spectra.
+#include "band.hpp"
 #include "fftsplit_internal.hpp"
 #include "fft_regs.hpp"
 #include "launch_util.hpp"
@@ -246,6 +247,252 @@ __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux
     y[(size_t(plane) * h + r) * w + c] = v;
 }
 
+
+// Overlap-save inverse transform writing whole row bands (width a multiple
+// of 4, at most 256).  Same work items and transforms as inverse_kernel;
+// what changes is the memory traffic and how items overlap:
+//   * the output spectra of item i+1 are loaded into registers while item
+//     i is transformed and stored;
+//   * the column pass runs one instruction stream in every lane: lane j = 0,
+//     which rebuilds the two Hermitian columns k2 = 0 and k2 = L/2 and packs
+//     them as one complex sequence, does so with selects, so no wave
+//     executes two paths;
+//   * the crops (T x T tiles, eq. 10) are placed in an LDS band of whole
+//     output rows (band.hpp, no halo; pitch `obp`, odd) and the band is
+//     written with 16-byte stores, lanes along each row, with bias and ReLU;
+//     in the first and last tile row of an item only the columns of its own
+//     tiles are written;
+//   * LDS strides are odd, so the lanes of a wave spread over the banks.
+template <int L, int TG, int NV>
+__global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
+    const float2* __restrict__ ys, const float* __restrict__ bias, float* __restrict__ y, int cout, int coutp, int h,
+    int w, int T, int th, int tw, int nt, int ntp, int ngroups, int nitems, int ipw, int obp, int relu,
+    unsigned y_bytes, float inv_h, float inv_tw, float inv_th) {
+    constexpr int H2 = L / 2, NT = TG * H2, NW = NT / 64, TP = H2 + 1;
+    constexpr int TTS = band_half_stride(L);  // half-spectrum patch stride (float2), odd
+    constexpr int F = stored_bins(L);
+    extern __shared__ float4 lds_raw[];
+    float2* tb = reinterpret_cast<float2*>(lds_raw);
+    float* ob = reinterpret_cast<float*>(lds_raw);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const BufRsrc ry = make_rsrc(ys, unsigned(size_t(coutp) * ntp * 8 * F));
+    const BufRsrc ryo = make_rsrc(y, y_bytes);
+    const unsigned bs8 = unsigned(coutp) * unsigned(ntp) * 8u;
+    auto opaque = [](int v) {
+        asm volatile("" : "+v"(v));
+        return v;
+    };
+
+    const int lw = xcd_logical_block(blockIdx.x, gridDim.x);
+    const int ibeg = lw * ipw;
+    const int iend = min(ibeg + ipw, nitems);
+
+    // column-pass roles: patch uc (fastest across lanes), column j
+    const int uc = tid % TG;
+    const int jc = tid / TG;
+    const bool j0 = jc == 0;
+    // Lane jc >= 1 needs column k2 = jc (bins mid(k1, jc), k1 < L); lane 0
+    // the halves k1 <= L/2 of the columns k2 = 0 and L/2.  Both are read as
+    // two runs of L/2 + 1 bins: pa[k1] and pb[k1] (pb[L/2] only for lane 0).
+    float2 pa[H2 + 1], pb[H2 + 1];
+    auto load_spectra = [&](int item) {
+        int co = 0, t0 = 0;
+        bool ok = false;
+        if (item >= 0) {
+            co = item / ngroups;
+            t0 = (item - co * ngroups) * TG;
+            ok = true;
+        }
+        const unsigned lane8 = unsigned(co * ntp + t0 + opaque(uc)) * 8u;
+        const unsigned va = ok ? lane8 + unsigned(j0 ? bin_col0(L, 0) : bin_mid(L, 0, jc)) * bs8 : kOutOfRange;
+        const unsigned vb = ok ? lane8 + unsigned(j0 ? bin_colh(L, 0) : bin_mid(L, H2, jc)) * bs8 : kOutOfRange;
+#pragma unroll
+        for (int k1 = 0; k1 <= H2; ++k1) {
+            pa[k1] = buf_load_f32x2(ry, va, unsigned(k1) * bs8);
+            pb[k1] = buf_load_f32x2(ry, k1 < H2 || j0 ? vb : kOutOfRange, unsigned(k1) * bs8);
+        }
+    };
+
+    // store-phase roles: lanes along a band row, 16 bytes each
+    const int w4 = w >> 2;
+    const int rpi = 64 / w4;
+    const int lrow = lane / w4;
+    const int c4 = lane - lrow * w4;
+    const int slot0 = wv * rpi + lrow;
+    const int slot_step = NW * rpi;
+    const unsigned cross4 = unsigned(cout - 1) * unsigned(h) * unsigned(w) * 4u;
+    const int dq = slot_step / h, dr = slot_step - dq * h;
+
+    auto process = [&](int item) {
+        const int co = item / ngroups;
+        const int t0 = (item - co * ngroups) * TG;
+        const BandGeom g = band_geom(t0, TG, nt, h, T, 0, th, tw);
+
+        // column pass
+        {
+            float2 cz[L];
+#pragma unroll
+            for (int k1 = 0; k1 < L; ++k1) {
+                float2 v0, v1;
+                if (k1 <= H2) {  // lane 0: U = Y0 + i YH
+                    const float2 a = pa[k1], b = pb[k1];
+                    v0 = make_float2(a.x - b.y, a.y + b.x);
+                } else {         // lane 0: Y0[k1] = conj(Y0[L-k1]), likewise YH
+                    const float2 a = pa[L - k1], b = pb[L - k1];
+                    v0 = make_float2(a.x + b.y, b.x - a.y);
+                }
+                v1 = k1 < H2 ? pa[k1] : pb[k1 - H2];
+                cz[k1] = j0 ? v0 : v1;
+            }
+            // the next item's spectra stay in flight through this item
+            load_spectra(item + 1 < iend ? item + 1 : -1);
+            fft<L, true>(cz);
+            float2* cbw = tb + opaque(uc * TTS);
+#pragma unroll
+            for (int m = 0; m < L; ++m) {
+                cbw[m * TP + jc] = j0 ? make_float2(cz[m].x, 0.f) : cz[m];
+                if (j0) cbw[m * TP + H2] = make_float2(cz[m].y, 0.f);
+            }
+        }
+        __syncthreads();
+
+        // row pass (j fastest across lanes) and placement of the crop in the band
+        {
+            const int j = tid % H2;
+            const int u = tid / H2;
+            float2 z[L];
+            const float2* ra = tb + opaque(u * TTS + 2 * j * TP);
+            const float2* rb = ra + TP;
+#pragma unroll
+            for (int k2 = 0; k2 < L; ++k2) {
+                if (k2 <= H2) {
+                    const float2 a = ra[k2], b = rb[k2];
+                    z[k2] = make_float2(a.x - b.y, a.y + b.x);
+                } else {
+                    const float2 a = ra[L - k2], b = rb[L - k2];
+                    z[k2] = make_float2(a.x + b.y, b.x - a.y);
+                }
+            }
+            __syncthreads();  // the output band reuses the half-spectrum LDS
+            fft<L, true>(z);
+            const int t = t0 + u;
+            if (t < nt && 2 * j < T) {
+                const int tr = div_small(t, tw, inv_tw);
+                const int b = t - tr * tw;
+                const int img = div_small(tr, th, inv_th);
+                const int a = tr - img * th;
+                const int r = a * T + 2 * j;
+                // rows run through the images in order: row r of image
+                // img0 + sg sits at slot sg * h + r - r0
+                const int sl = __umul24(img - g.img0, h) - g.r0 + r;
+                const bool ok0 = r < h;
+                const bool ok1 = r + 1 < h && 2 * j + 1 < T;
+                float* d = ob + opaque(sl * obp + b * T);
+#pragma unroll
+                for (int q = 0; q < L; ++q) {
+                    if (q < T) {
+                        if (ok0) d[q] = z[q].x;
+                        if (ok1) d[obp + q] = z[q].y;
+                    }
+                }
+            }
+        }
+        __syncthreads();
+
+        // store phase: whole band rows, bias and ReLU
+        {
+            const float bv = bias ? bias[co] : 0.f;
+            const int tl = (t0 + TG < nt ? t0 + TG : nt) - 1;
+            const int tr0 = t0 / tw, tr1 = tl / tw;
+            // columns of this item's tiles in its first and last tile rows
+            const int lo0 = (t0 - tr0 * tw) * T;
+            const int hi_last = min((tl - tr1 * tw + 1) * T, w);
+            const int rows_first = min(T, h - (tr0 % th) * T);
+            const int rows_last = min(T, h - (tr1 % th) * T);
+            const int sl0 = opaque(slot0);
+            const int x0 = sl0 + g.r0;
+            int qd = div_small(x0, h, inv_h);
+            int rr = x0 - qd * h;
+            unsigned voff = unsigned((((g.img0 * cout + co) * h + g.r0) * w) * 4) + unsigned(sl0 * w * 4) +
+                            unsigned(16 * c4) + unsigned(qd) * cross4;
+            const unsigned dq_off = unsigned(dq) * cross4;
+            const float* src = ob + sl0 * obp + 4 * c4;
+            // Every lane issues one 16-byte store per slot (dropped through an
+            // out-of-range offset where it has nothing to write), so the count
+            // of stores after this item's spectrum loads is fixed; only a
+            // float4 that straddles an item's first or last column takes
+            // four 4-byte stores.
+#pragma unroll
+            for (int k = 0; k < NV; ++k) {
+                const int sl = sl0 + k * slot_step;
+                const bool ok = lrow < rpi && sl < g.slots;
+                int lo = 0, hi = w;
+                if (sl < rows_first) {
+                    lo = lo0;
+                    if (tr1 == tr0) hi = hi_last;
+                } else if (sl >= g.slots - rows_last) {
+                    hi = hi_last;
+                }
+                const float* sp = ok ? src + k * slot_step * obp : ob;
+                float4 v = make_float4(sp[0] + bv, sp[1] + bv, sp[2] + bv, sp[3] + bv);
+                if (relu) v = make_float4(fmaxf(v.x, 0.f), fmaxf(v.y, 0.f), fmaxf(v.z, 0.f), fmaxf(v.w, 0.f));
+                const int col = 4 * c4;
+                const unsigned soff = unsigned(k * slot_step * w * 4);
+                const bool full = ok && col >= lo && col + 4 <= hi;
+                buf_store_f32x4(v, ryo, full ? voff : kOutOfRange, soff);
+                if (ok && !full && col + 4 > lo && col < hi) {
+                    buf_store_f32(v.x, ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
+                    buf_store_f32(v.y, ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
+                    buf_store_f32(v.z, ryo, col + 2 >= lo && col + 2 < hi ? voff + 8u : kOutOfRange, soff);
+                    buf_store_f32(v.w, ryo, col + 3 >= lo && col + 3 < hi ? voff + 12u : kOutOfRange, soff);
+                }
+                rr += dr;
+                voff += dq_off;
+                const bool carry = rr >= h;
+                rr -= carry ? h : 0;
+                voff += carry ? cross4 : 0u;
+            }
+        }
+        __syncthreads();  // the next item's column pass reuses the band's LDS
+    };
+
+    // The first item is peeled off the loop so that, inside the loop, the
+    // wait for an item's spectra leaves the previous item's stores in flight.
+    if (ibeg < iend) {
+        load_spectra(ibeg);
+        process(ibeg);
+        for (int item = ibeg + 1; item < iend; ++item) process(item);
+    }
+}
+
+template <int L, int TG, int NV>
+static hipError_t launch_inverse_band(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y,
+                                      hipStream_t s, const LaunchEvents& ev) {
+    constexpr int NT = TG * (L / 2);
+    auto kern = inverse_band_kernel<L, TG, NV>;
+    const int lds = p.inv_lds;
+    if (lds > 64 * 1024) {
+        const hipError_t attr = allow_dynamic_lds(kern, lds);
+        if (attr != hipSuccess) return attr;
+    }
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern), NT, lds) !=
+            hipSuccess ||
+        per_cu < 1)
+        per_cu = 1;
+    const int ngroups = p.ntp / TG;
+    const int nitems = ngroups * p.prob.cout;
+    const int ipw = items_per_workgroup(nitems, p.cus * per_cu);
+    const dim3 grid(unsigned((nitems + ipw - 1) / ipw));
+    const unsigned y_bytes = unsigned(size_t(p.prob.n) * p.prob.cout * p.prob.h * p.prob.w * 4);
+    return launch_kernel(kern, grid, dim3(NT), unsigned(lds), s, ev.start, ev.stop, ys, bias, y, p.prob.cout, p.coutp,
+                         p.prob.h, p.prob.w, p.T, p.th, p.tw, p.nt, p.ntp, ngroups, nitems, ipw, p.inv_obp,
+                         int(p.relu), y_bytes, 1.0f / float(p.prob.h), 1.0f / float(p.tw), 1.0f / float(p.th));
+}
+
 template <int L, int TG, bool OAA>
 static hipError_t launch_inverse_v(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y,
                                    float* aux, hipStream_t s, const LaunchEvents& ev) {
@@ -275,6 +522,14 @@ hipError_t launch_inverse(const fftsplit_plan_s& p, const float2* ys, const floa
                           hipStream_t s, const LaunchEvents& ev) {
     float* a = static_cast<float*>(aux);
     if (p.oaa && !a) return hipErrorInvalidValue;
+    if (p.inv_band) {
+        switch (p.L) {
+            case 8: return launch_inverse_band<8, 64, kBandNV8>(p, ys, bias, y, s, ev);
+            case 16: return launch_inverse_band<16, 32, kBandNV16>(p, ys, bias, y, s, ev);
+            case 32: return launch_inverse_band<32, 16, kBandNV32>(p, ys, bias, y, s, ev);
+        }
+        return hipErrorInvalidValue;
+    }
     switch (p.L) {
         case 8: return launch_inverse_L<8, 64>(p, ys, bias, y, a, s, ev);
         case 16: return launch_inverse_L<16, 32>(p, ys, bias, y, a, s, ev);

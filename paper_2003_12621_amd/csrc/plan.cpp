@@ -73,6 +73,39 @@ static Geometry geometry(const fftsplit_problem_t& p, int L) {
 
 static bool supported_L(int L) { return L == 8 || L == 16 || L == 32; }
 
+// The band variant of the inverse transform (overlap-save, width a multiple
+// of 4 and at most 256): used when the output band of any work item fits the
+// store slots it assigns and its LDS stays within two workgroups per compute
+// unit.  FFTSPLIT_INVERSE_BAND=0 turns it off.
+static void choose_inverse_band(fftsplit_plan_s& p) {
+    p.inv_band = false;
+    const int w = p.prob.w, L = p.L, T = p.T;
+    if (p.oaa || w % 4 != 0 || w > 256 || p.nt >= (1 << 22) || p.prob.h >= (1 << 22) ||
+        p.yspec_bytes >= (size_t(1) << 31))
+        return;
+    if (const char* e = std::getenv("FFTSPLIT_INVERSE_BAND"))
+        if (*e == '0') return;
+    const int tg = patch_group(L);
+    const int nw = tg * (L / 2) / 64;
+    const int rpi = 64 / (w / 4);
+    const int nv = L == 8 ? kBandNV8 : (L == 16 ? kBandNV16 : kBandNV32);
+    int slots = 0;
+    for (int t0 = 0; t0 < p.nt; t0 += tg) {
+        const BandGeom g = band_geom(t0, tg, p.nt, p.prob.h, T, 0, p.th, p.tw);
+        if (g.slots > slots) slots = g.slots;
+    }
+    if ((slots + nw * rpi - 1) / (nw * rpi) > nv) return;
+    int obp = p.tw * T;
+    if (obp % 2 == 0) ++obp;   // odd pitch: a patch's row-pass lanes write distinct banks
+    const size_t band = size_t(slots) * obp * 4;
+    const size_t half = size_t(tg) * band_half_stride(L) * 8;
+    const size_t lds = band > half ? band : half;
+    if (lds > 80 * 1024) return;
+    p.inv_band = true;
+    p.inv_obp = obp;
+    p.inv_lds = int(lds);
+}
+
 // The band variant of the forward transform (overlap-save, image width a
 // multiple of 4 and at most 256) is used when its band of any work item fits
 // the registers it prefetches into and its LDS stays within two workgroups
@@ -267,6 +300,7 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     }
 
     choose_forward_band(*plan);
+    choose_inverse_band(*plan);
 
     const char* log = std::getenv("FFTSPLIT_LOG");
     if (log && *log && *log != '0') {
