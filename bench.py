@@ -38,8 +38,9 @@ def algorithmic_counts(layer, info):
     """Algorithmic bytes/flops of each kernel per launch (one batch).
 
     forward : read x once + write the patch spectra once
-    contract: 8 flops per complex multiply-add, over every stored bin,
-              padded patch and padded output channel the kernel computes
+    contract: 8 flops per complex multiply-add over the stored complex bins,
+              and 2 per real multiply-add for the two slots that each hold
+              two real bins, per (patch, input channel, output channel)
     inverse : read the output spectra once + write y once
     """
     F, ntp, coutp = info.bins, info.tiles_padded, info.cout_padded
@@ -48,7 +49,7 @@ def algorithmic_counts(layer, info):
     y_bytes = 4 * layer.n * layer.cout * layer.h * layer.w
     return {
         "forward_bytes": x_bytes + 8 * F * layer.cin * nt,
-        "contract_flops": 8 * F * layer.cin * layer.cout * nt,
+        "contract_flops": (8 * (F - 2) + 2 * 2 * 2) * layer.cin * layer.cout * nt,
         "contract_bytes": 8 * F * (layer.cin * nt + layer.cin * layer.cout + layer.cout * nt),
         "inverse_bytes": 8 * F * layer.cout * nt + y_bytes,
     }

@@ -80,13 +80,18 @@ typedef struct {
 
 /* What a plan decided.  Spectra are complex64 (re, im float pairs).
  *
- * Frequency bins: the 2-D real transform of an L x L patch has L*(L/2+1)
- * bins (k1 in [0,L), k2 in [0,L/2]); columns k2 = 0 and k2 = L/2 are
- * Hermitian in k1, so only their k1 <= L/2 halves are kept, leaving
- * bins = L*L/2 + 2.  Bin index f enumerates
- *   f = (k2-1)*L + k1                 for k2 in [1, L/2-1], k1 in [0, L)
- *   f = L*(L/2-1) + k1                for k2 = 0,   k1 in [0, L/2]
- *   f = L*(L/2-1) + L/2+1 + k1        for k2 = L/2, k1 in [0, L/2]
+ * Frequency bins: the 2-D real transform S of an L x L patch has
+ * L*(L/2+1) bins (k1 in [0,L), k2 in [0,L/2]); columns k2 = 0 and k2 = L/2
+ * are Hermitian in k1, so only their k1 <= L/2 halves are kept, and the
+ * four of those that are real (k1, k2 in {0, L/2}) share two slots, leaving
+ * bins = L*L/2 slots.  Slot f holds
+ *   f = (k2-1)*L + k1             S(k1, k2)   for k2 in [1, L/2-1], k1 in [0, L)
+ *   f = L*(L/2-1) + k1 - 1        S(k1, 0)    for k1 in [1, L/2-1]
+ *   f = L*(L/2-1) + L/2-2 + k1    S(k1, L/2)  for k1 in [1, L/2-1]
+ *   f = L*L/2 - 2                 (S(0, 0), S(L/2, 0))     as (re, im)
+ *   f = L*L/2 - 1                 (S(0, L/2), S(L/2, L/2)) as (re, im)
+ * The two last slots are multiplied part by part in the per-bin product
+ * (a product of two real bins is real), the others as complex numbers.
  *
  * Patch index t = (img * tiles_h + a) * tiles_w + b for the patch whose
  * top-left output pixel is (a*T, b*T); t in [tiles, tiles_padded) are zero
@@ -105,7 +110,7 @@ typedef struct {
     int tiles_h, tiles_w;/* ceil(h/T), ceil(w/T) */
     int tiles;           /* n * tiles_h * tiles_w */
     int tiles_padded;    /* tiles rounded up to the contraction's tile granularity */
-    int bins;            /* L*L/2 + 2 */
+    int bins;            /* L*L/2 */
     int cout_padded;     /* cout rounded up to the contraction's tile granularity */
     unsigned flags;
     size_t wspec_bytes;

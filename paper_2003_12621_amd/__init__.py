@@ -279,14 +279,19 @@ def maxpool2x2(x, out=None):
 
 
 def bin_coords(L: int):
-    """(k1, k2) of each stored bin, in the library's bin order (fftsplit.h)."""
+    """Stored bins of an L x L real transform, in the library's order
+    (fftsplit.h): a list of L*L/2 entries.  Entry f is (k1, k2) for a complex
+    bin; the last two entries are pairs ((k1, k2) of the real part,
+    (k1, k2) of the imaginary part) for the slots holding two real bins."""
     h2 = L // 2
     coords = []
     for k2 in range(1, h2):
         for k1 in range(L):
             coords.append((k1, k2))
-    for k1 in range(h2 + 1):
+    for k1 in range(1, h2):
         coords.append((k1, 0))
-    for k1 in range(h2 + 1):
+    for k1 in range(1, h2):
         coords.append((k1, h2))
+    coords.append(((0, 0), (h2, 0)))
+    coords.append(((0, h2), (h2, h2)))
     return coords

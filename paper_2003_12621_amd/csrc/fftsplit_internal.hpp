@@ -56,13 +56,20 @@ constexpr int kBandNV8 = 8;
 constexpr int kBandNV16 = 8;
 constexpr int kBandNV32 = 16;
 
-// Number of stored frequency bins of an L x L real transform.
-__host__ __device__ constexpr int stored_bins(int L) { return L * L / 2 + 2; }
-
-// Bin index of (k1, k2) for k2 in [1, L/2-1]; and of the two real columns.
+// Stored frequency bins of an L x L real transform: L*L/2 (layout in
+// fftsplit.h).  Bins with k2 in [1, L/2-1] (all k1) are stored as they are;
+// of the columns k2 = 0 and k2 = L/2, which are Hermitian in k1, the
+// complex bins k1 in [1, L/2-1] are stored, and their four real bins
+// (k1, k2 in {0, L/2}) share two slots: real_a = (S(0,0), S(L/2,0)),
+// real_b = (S(0,L/2), S(L/2,L/2)) as (re, im).
+__host__ __device__ constexpr int stored_bins(int L) { return L * L / 2; }
 __host__ __device__ constexpr int bin_mid(int L, int k1, int k2) { return (k2 - 1) * L + k1; }
-__host__ __device__ constexpr int bin_col0(int L, int k1) { return L * (L / 2 - 1) + k1; }
-__host__ __device__ constexpr int bin_colh(int L, int k1) { return L * (L / 2 - 1) + L / 2 + 1 + k1; }
+// complex bins of the real columns, k1 in [1, L/2-1]
+__host__ __device__ constexpr int bin_col0(int L, int k1) { return L * (L / 2 - 1) + k1 - 1; }
+__host__ __device__ constexpr int bin_colh(int L, int k1) { return L * (L / 2 - 1) + L / 2 - 1 + k1 - 1; }
+// the two slots holding pairs of real bins
+__host__ __device__ constexpr int bin_real_a(int L) { return L * L / 2 - 2; }
+__host__ __device__ constexpr int bin_real_b(int L) { return L * L / 2 - 1; }
 
 // Thread-local error detail for fftsplit_last_error().
 void set_error(const std::string& msg);

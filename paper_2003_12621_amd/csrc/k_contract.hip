@@ -13,6 +13,10 @@
 // so every operand fragment is 32 consecutive complex values of one input
 // channel row, and every stored output row is 32 consecutive patches.
 //
+// The last two bins each hold two real bins (re, im) -- the four real bins
+// of the two Hermitian columns, fftsplit.h -- whose products are taken
+// component by component: Y = (sum Wr Xr, sum Wi Xi).
+//
 // With G3 the complex product takes three real products instead (Gauss):
 //     P1 = Wr Xr, P2 = Wi Xi, P3 = (Wr + Wi)(Xr + Xi);  Y = (P1 - P2, P3 - P1 - P2)
 // which cuts the matrix-core work by a quarter for two vector adds per
@@ -52,7 +56,7 @@ struct ConShape {
 template <int BM, int BN, int KC, int WM, bool G3>
 __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict__ xs, const float2* __restrict__ ws,
                                                        float2* __restrict__ ys, int cin, int coutp, int ntp,
-                                                       int nbco, int nbt) {
+                                                       int nbco, int nbt, int nbins) {
     using S = ConShape<BM, BN, KC, WM>;
     constexpr int TM = S::TM, TN = S::TN;
     extern __shared__ float4 lds_raw[];
@@ -68,6 +72,9 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     const int rest = lb / nbco;
     const int tbk = rest % nbt;
     const int f = rest / nbt;
+    // the last two bins are slots of two real bins each (fftsplit.h): their
+    // products are taken component by component
+    const bool packed = f >= nbins - 2;
     const int co0 = cbk * BM;
     const int t0 = tbk * BN;
 
@@ -180,16 +187,18 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
             } else {
 #pragma unroll
                 for (int i = 0; i < TM; ++i) {
-                    const float ar = a[cur][i].x, ai = a[cur][i].y, nai = -ai;
+                    // a slot of two real bins: accR = sum Wr Xr, accI = sum Wi Xi
+                    const float ar = a[cur][i].x, ai = a[cur][i].y;
+                    const float a2 = packed ? ai : ar, nai = packed ? 0.f : -ai, ai4 = packed ? 0.f : ai;
 #pragma unroll
                     for (int j = 0; j < TN; ++j) {
                         accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ar, b[cur][j].x, accR[i][j], 0, 0, 0);
-                        accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ar, b[cur][j].y, accI[i][j], 0, 0, 0);
+                        accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a2, b[cur][j].y, accI[i][j], 0, 0, 0);
                     }
 #pragma unroll
                     for (int j = 0; j < TN; ++j) {
                         accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(nai, b[cur][j].y, accR[i][j], 0, 0, 0);
-                        accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ai, b[cur][j].x, accI[i][j], 0, 0, 0);
+                        accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ai4, b[cur][j].x, accI[i][j], 0, 0, 0);
                     }
                 }
             }
@@ -209,7 +218,8 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
                 const int ii = 8 * (r >> 2) + 4 * krow + (r & 3);
                 if (G3) {
                     const float p1 = accR[i][j][r], p2 = accI[i][j][r];
-                    yb[size_t(ii) * ntp] = make_float2(p1 - p2, acc3[G3 ? i : 0][G3 ? j : 0][r] - p1 - p2);
+                    yb[size_t(ii) * ntp] = packed ? make_float2(p1, p2)
+                                                  : make_float2(p1 - p2, acc3[G3 ? i : 0][G3 ? j : 0][r] - p1 - p2);
                 } else {
                     yb[size_t(ii) * ntp] = make_float2(accR[i][j][r], accI[i][j][r]);
                 }
@@ -229,7 +239,7 @@ static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, 
     const int nbco = p.coutp / BM, nbt = p.ntp / BN;
     const size_t nb = size_t(nbco) * nbt * p.bins;
     return launch_kernel(kern, dim3(unsigned(nb)), dim3(S::NT), S::LDS_BYTES, s, ev.start, ev.stop, xs, ws, ys,
-                         p.prob.cin, p.coutp, p.ntp, nbco, nbt);
+                         p.prob.cin, p.coutp, p.ntp, nbco, nbt, p.bins);
 }
 
 hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xs, const float2* ws, float2* ys,

@@ -173,10 +173,16 @@ __global__ __launch_bounds__(TG * (L / 2)) void forward_kernel(const float* __re
             // scalar offset (always in range).
             const unsigned voff = unsigned(c * ntp + t0 + u) * 8u;
             if (j == 0) {
+                // the real bins (k1 = 0, L/2) of both columns share two slots
+                float2 a0, b0, ah, bh;
+                split_two_real(cz[0], cz[0], a0, b0);
+                split_two_real(cz[H2], cz[H2], ah, bh);
+                buf_store_f32x2(make_float2(a0.x, ah.x), rx, voff, unsigned(bin_real_a(L)) * bs8);
+                buf_store_f32x2(make_float2(b0.x, bh.x), rx, voff, unsigned(bin_real_b(L)) * bs8);
 #pragma unroll
-                for (int k1 = 0; k1 <= H2; ++k1) {
+                for (int k1 = 1; k1 < H2; ++k1) {
                     float2 a, b;
-                    split_two_real(cz[k1], cz[(L - k1) % L], a, b);
+                    split_two_real(cz[k1], cz[L - k1], a, b);
                     buf_store_f32x2(a, rx, voff, unsigned(bin_col0(L, k1)) * bs8);
                     buf_store_f32x2(b, rx, voff, unsigned(bin_colh(L, k1)) * bs8);
                 }
@@ -388,18 +394,27 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
             }
             __syncthreads();  // the next item's band reuses the half-spectrum LDS
             fft<L, false>(cz);
+            // Lane j >= 1 stores bins (k1, j) and (k1 + L/2, j); lane 0 the
+            // complex bins k1 in [1, L/2-1] of the two real columns, and at
+            // k1 = 0 their four real bins packed into two slots.
             const unsigned lane8 = unsigned(c * ntp + t0 + u) * 8u;
-            const unsigned va = lane8 + unsigned(j0 ? bin_col0(L, 0) : bin_mid(L, 0, j)) * bs8;
-            const unsigned vb = lane8 + unsigned(j0 ? bin_colh(L, 0) : bin_mid(L, H2, j)) * bs8;
+            const unsigned va0 = lane8 + unsigned(j0 ? bin_real_a(L) : bin_mid(L, 0, j)) * bs8;
+            const unsigned vb0 = lane8 + unsigned(j0 ? bin_real_b(L) : bin_mid(L, H2, j)) * bs8;
+            const unsigned va = lane8 + unsigned(j0 ? bin_col0(L, 1) - 1 : bin_mid(L, 0, j)) * bs8;
+            const unsigned vb = lane8 + unsigned(j0 ? bin_colh(L, 1) - 1 : bin_mid(L, H2, j)) * bs8;
+            {
+                float2 sa0, sb0, sah, sbh;
+                split_two_real(cz[0], cz[0], sa0, sb0);
+                split_two_real(cz[H2], cz[H2], sah, sbh);
+                buf_store_f32x2(j0 ? make_float2(sa0.x, sah.x) : cz[0], rx, va0, 0);
+                buf_store_f32x2(j0 ? make_float2(sb0.x, sbh.x) : cz[H2], rx, vb0, 0);
+            }
 #pragma unroll
-            for (int k1 = 0; k1 <= H2; ++k1) {
+            for (int k1 = 1; k1 < H2; ++k1) {
                 float2 sa, sb;
-                split_two_real(cz[k1], cz[(L - k1) % L], sa, sb);
+                split_two_real(cz[k1], cz[L - k1], sa, sb);
                 buf_store_f32x2(j0 ? sa : cz[k1], rx, va, unsigned(k1) * bs8);
-                if (k1 < H2)
-                    buf_store_f32x2(j0 ? sb : cz[k1 + H2], rx, vb, unsigned(k1) * bs8);
-                else  // bin (L/2, L/2) exists only for the real columns
-                    buf_store_f32x2(sb, rx, j0 ? vb : kOutOfRange, unsigned(k1) * bs8);
+                buf_store_f32x2(j0 ? sb : cz[k1 + H2], rx, vb, unsigned(k1) * bs8);
             }
         }
     };

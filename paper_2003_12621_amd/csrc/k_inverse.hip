@@ -99,8 +99,15 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
         float2 cz[L];
         if (j == 0) {
             float2 y0[H2 + 1], yh[H2 + 1];
+            // the real bins (k1 = 0, L/2) of both columns share two slots
+            const float2 ra = buf_load_f32x2(ry, voff, unsigned(bin_real_a(L)) * bs8);
+            const float2 rb = buf_load_f32x2(ry, voff, unsigned(bin_real_b(L)) * bs8);
+            y0[0] = make_float2(ra.x, 0.f);
+            y0[H2] = make_float2(ra.y, 0.f);
+            yh[0] = make_float2(rb.x, 0.f);
+            yh[H2] = make_float2(rb.y, 0.f);
 #pragma unroll
-            for (int k1 = 0; k1 <= H2; ++k1) {
+            for (int k1 = 1; k1 < H2; ++k1) {
                 y0[k1] = buf_load_f32x2(ry, voff, unsigned(bin_col0(L, k1)) * bs8);
                 yh[k1] = buf_load_f32x2(ry, voff, unsigned(bin_colh(L, k1)) * bs8);
             }
@@ -294,10 +301,12 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     const int uc = tid % TG;
     const int jc = tid / TG;
     const bool j0 = jc == 0;
-    // Lane jc >= 1 needs column k2 = jc (bins mid(k1, jc), k1 < L); lane 0
-    // the halves k1 <= L/2 of the columns k2 = 0 and L/2.  Both are read as
-    // two runs of L/2 + 1 bins: pa[k1] and pb[k1] (pb[L/2] only for lane 0).
-    float2 pa[H2 + 1], pb[H2 + 1];
+    // Lane jc >= 1 needs column k2 = jc: pa[k1] = bin (k1, jc) and
+    // pb[k1] = bin (k1 + L/2, jc), k1 < L/2.  Lane 0 needs the halves
+    // k1 <= L/2 of the real columns k2 = 0 and L/2: pa[0] and pb[0] are the
+    // two slots of their real bins, pa[k1] and pb[k1] (k1 >= 1) their
+    // complex bins k1.
+    float2 pa[H2], pb[H2];
     auto load_spectra = [&](int item) {
         int co = 0, t0 = 0;
         bool ok = false;
@@ -307,12 +316,16 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
             ok = true;
         }
         const unsigned lane8 = unsigned(co * ntp + t0 + opaque(uc)) * 8u;
-        const unsigned va = ok ? lane8 + unsigned(j0 ? bin_col0(L, 0) : bin_mid(L, 0, jc)) * bs8 : kOutOfRange;
-        const unsigned vb = ok ? lane8 + unsigned(j0 ? bin_colh(L, 0) : bin_mid(L, H2, jc)) * bs8 : kOutOfRange;
+        const unsigned va0 = ok ? lane8 + unsigned(j0 ? bin_real_a(L) : bin_mid(L, 0, jc)) * bs8 : kOutOfRange;
+        const unsigned vb0 = ok ? lane8 + unsigned(j0 ? bin_real_b(L) : bin_mid(L, H2, jc)) * bs8 : kOutOfRange;
+        const unsigned va = ok ? lane8 + unsigned(j0 ? bin_col0(L, 1) - 1 : bin_mid(L, 0, jc)) * bs8 : kOutOfRange;
+        const unsigned vb = ok ? lane8 + unsigned(j0 ? bin_colh(L, 1) - 1 : bin_mid(L, H2, jc)) * bs8 : kOutOfRange;
+        pa[0] = buf_load_f32x2(ry, va0, 0);
+        pb[0] = buf_load_f32x2(ry, vb0, 0);
 #pragma unroll
-        for (int k1 = 0; k1 <= H2; ++k1) {
+        for (int k1 = 1; k1 < H2; ++k1) {
             pa[k1] = buf_load_f32x2(ry, va, unsigned(k1) * bs8);
-            pb[k1] = buf_load_f32x2(ry, k1 < H2 || j0 ? vb : kOutOfRange, unsigned(k1) * bs8);
+            pb[k1] = buf_load_f32x2(ry, vb, unsigned(k1) * bs8);
         }
     };
 
@@ -333,18 +346,25 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
 
         // column pass
         {
+            // lane 0: column spectra Y0[k1], YH[k1] for k1 <= L/2
+            auto y0 = [&](int k) {
+                return k == 0 ? make_float2(pa[0].x, 0.f) : (k == H2 ? make_float2(pa[0].y, 0.f) : pa[k]);
+            };
+            auto yh = [&](int k) {
+                return k == 0 ? make_float2(pb[0].x, 0.f) : (k == H2 ? make_float2(pb[0].y, 0.f) : pb[k]);
+            };
             float2 cz[L];
 #pragma unroll
             for (int k1 = 0; k1 < L; ++k1) {
-                float2 v0, v1;
+                float2 v0;
                 if (k1 <= H2) {  // lane 0: U = Y0 + i YH
-                    const float2 a = pa[k1], b = pb[k1];
+                    const float2 a = y0(k1), b = yh(k1);
                     v0 = make_float2(a.x - b.y, a.y + b.x);
                 } else {         // lane 0: Y0[k1] = conj(Y0[L-k1]), likewise YH
-                    const float2 a = pa[L - k1], b = pb[L - k1];
+                    const float2 a = y0(L - k1), b = yh(L - k1);
                     v0 = make_float2(a.x + b.y, b.x - a.y);
                 }
-                v1 = k1 < H2 ? pa[k1] : pb[k1 - H2];
+                const float2 v1 = k1 < H2 ? pa[k1] : pb[k1 - H2];
                 cz[k1] = j0 ? v0 : v1;
             }
             // the next item's spectra stay in flight through this item

@@ -32,30 +32,46 @@ __global__ __launch_bounds__(256) void weights_kernel(const float* __restrict__ 
         wspec[idx] = make_float2(0.f, 0.f);
         return;
     }
-    // Decode the bin (k1, k2) from f (order documented in fftsplit.h).
+    // Decode the bin from f (order documented in fftsplit.h).  A slot of
+    // the real bins holds the (real) values of two bins: (k1, k2) in its
+    // real part and (k1b, k2b) in its imaginary part.
     const int h2 = L / 2;
-    int k1, k2;
+    int k1, k2, k1b = -1, k2b = -1;
     if (f < L * (h2 - 1)) {
         k2 = 1 + f / L;
         k1 = f % L;
-    } else if (f < L * (h2 - 1) + h2 + 1) {
+    } else if (f < L * (h2 - 1) + h2 - 1) {
         k2 = 0;
-        k1 = f - L * (h2 - 1);
-    } else {
+        k1 = f - L * (h2 - 1) + 1;
+    } else if (f < L * h2 - 2) {
         k2 = h2;
-        k1 = f - L * (h2 - 1) - (h2 + 1);
+        k1 = f - L * (h2 - 1) - (h2 - 1) + 1;
+    } else {
+        k1 = 0;
+        k1b = h2;
+        k2 = k2b = f == L * h2 - 2 ? 0 : h2;
     }
     const int step = kTwN / L;
     const float* wp = w + (size_t(co) * cin + ci) * K * K;
-    double re = 0.0, im = 0.0;
-    for (int u = 0; u < K; ++u) {
-        for (int v = 0; v < K; ++v) {
-            const int e = ((u * k1 + v * k2) % L) * step;
-            const double val = double(wp[u * K + v]);
-            // conj(sum w exp(-2 pi i e / L)) = sum w exp(+2 pi i e / L)
-            re += val * tw.c[e];
-            im += val * tw.s[e];
+    // conj(sum w exp(-2 pi i e / L)) = sum w exp(+2 pi i e / L), e = u k1 + v k2
+    auto spectrum = [&](int a, int b, double& re, double& im) {
+        re = 0.0;
+        im = 0.0;
+        for (int u = 0; u < K; ++u) {
+            for (int v = 0; v < K; ++v) {
+                const int e = ((u * a + v * b) % L) * step;
+                const double val = double(wp[u * K + v]);
+                re += val * tw.c[e];
+                im += val * tw.s[e];
+            }
         }
+    };
+    double re, im;
+    spectrum(k1, k2, re, im);
+    if (k1b >= 0) {   // two real bins: their imaginary parts are zero
+        double re2, im2;
+        spectrum(k1b, k2b, re2, im2);
+        im = re2;
     }
     const double inv = 1.0 / double(L * L);
     wspec[idx] = make_float2(float(re * inv), float(im * inv));

@@ -2,37 +2,53 @@
 arrays and the library's stored-bin layout (documented in fftsplit.h).
 
 Only index bookkeeping lives here -- no transform arithmetic: the stored
-bins are a subset of the full spectrum, and the rest follows from the
-Hermitian symmetry of a real array's spectrum, S[-k1, -k2] = conj(S[k1, k2]).
+bins are a subset of the full spectrum (the four real bins of the columns
+k2 = 0 and L/2 packed two to a slot, as real and imaginary part), and the
+rest follows from the Hermitian symmetry of a real array's spectrum,
+S[-k1, -k2] = conj(S[k1, k2]).
 """
 import numpy as np
 
 
 def stored_coords(L: int):
-    """(k1, k2) of every stored bin in the header's order."""
+    """(k1, k2) of every complex stored bin, in the header's order; the two
+    slots that follow them hold the real bins of real_pairs(L)."""
     h2 = L // 2
     out = [(k1, k2) for k2 in range(1, h2) for k1 in range(L)]
-    out += [(k1, 0) for k1 in range(h2 + 1)]
-    out += [(k1, h2) for k1 in range(h2 + 1)]
+    out += [(k1, 0) for k1 in range(1, h2)]
+    out += [(k1, h2) for k1 in range(1, h2)]
     return out
 
 
+def real_pairs(L: int):
+    """The last two stored slots: (bin in the real part, bin in the imaginary part)."""
+    h2 = L // 2
+    return [((0, 0), (h2, 0)), ((0, h2), (h2, h2))]
+
+
 def full_to_stored(full: np.ndarray) -> np.ndarray:
-    """[..., L, L] -> [bins, ...]."""
+    """[..., L, L] -> [bins, ...] (complex128)."""
     L = full.shape[-1]
     k1, k2 = np.array(stored_coords(L)).T
-    return np.moveaxis(full[..., k1, k2], -1, 0)
+    st = np.moveaxis(full[..., k1, k2], -1, 0).astype(np.complex128)
+    packed = [full[..., a[0], a[1]].real + 1j * full[..., b[0], b[1]].real for a, b in real_pairs(L)]
+    return np.concatenate([st, np.stack(packed)], axis=0)
 
 
 def stored_to_full(stored: np.ndarray, L: int) -> np.ndarray:
     """[bins, ...] -> [..., L, L], filling the unstored bins by symmetry."""
     coords = stored_coords(L)
+    nc = len(coords)
     lead = stored.shape[1:]
     full = np.zeros(lead + (L, L), dtype=np.complex128)
     have = np.zeros((L, L), dtype=bool)
     for f, (k1, k2) in enumerate(coords):
         full[..., k1, k2] = stored[f]
         have[k1, k2] = True
+    for i, (a, b) in enumerate(real_pairs(L)):
+        full[..., a[0], a[1]] = stored[nc + i].real
+        full[..., b[0], b[1]] = stored[nc + i].imag
+        have[a] = have[b] = True
     for k1 in range(L):
         for k2 in range(L):
             if not have[k1, k2]:

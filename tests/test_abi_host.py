@@ -47,7 +47,7 @@ def test_first_config_geometry():
     p = plan()
     i = p.info
     assert (i.tile, i.nfft, i.tiles_h, i.tiles_w, i.tiles) == (6, 8, 6, 6, 36)
-    assert i.bins == 8 * 8 // 2 + 2
+    assert i.bins == 8 * 8 // 2
     assert i.tiles_padded % 64 == 0 and i.tiles_padded >= 36
     assert i.cout_padded >= 16
     assert i.wspec_bytes == 8 * i.bins * 3 * i.cout_padded
@@ -141,12 +141,16 @@ def test_auto_tile_choice_and_env_override(monkeypatch):
 
 
 def test_bin_order_matches_header():
+    from spectra_layout import stored_coords, real_pairs
     for L in (8, 16, 32):
         coords = fs.bin_coords(L)
-        assert len(coords) == L * L // 2 + 2
-        assert len(set(coords)) == len(coords)
+        assert len(coords) == L * L // 2
+        assert coords[:-2] == stored_coords(L) and coords[-2:] == real_pairs(L)
+        stored = set(coords[:-2]) | {b for pair in coords[-2:] for b in pair}
+        assert len(stored) == L * L // 2 + 2
+        # the packed slots hold exactly the real bins: both indices in {0, L/2}
+        assert all(k in (0, L // 2) for pair in coords[-2:] for b in pair for k in b)
         # every (k1, k2) with k2 in [0, L/2] is stored or is the conjugate of a stored bin
-        stored = set(coords)
         for k1 in range(L):
             for k2 in range(L // 2 + 1):
                 mirror = ((-k1) % L, (-k2) % L)
@@ -161,7 +165,7 @@ def test_spectra_layout_helpers_roundtrip():
         a = rng.standard_normal((2, 3, L, L))
         full = np.fft.fft2(a)
         st = full_to_stored(full)
-        assert st.shape == (L * L // 2 + 2, 2, 3)
+        assert st.shape == (L * L // 2, 2, 3)
         np.testing.assert_allclose(stored_to_full(st, L), full, rtol=0, atol=1e-12)
     # the error measure sees imaginary parts
     assert rel_l2(np.array([1 + 1j]), np.array([1 + 0j])) == 1.0

@@ -94,6 +94,11 @@ def test_contraction(name, shape, tile):
     # filter spectra are already conjugated, so they enter as conj(W).
     ref = oracle.hadamard_channel_sum(X.transpose(2, 1, 0), np.conj(W).transpose(2, 1, 0))  # [t, co, bins]
     ref = ref.transpose(2, 1, 0)                                    # [bins, co, t]
+    # the last two slots each hold two real bins (real and imaginary part):
+    # their products are taken part by part
+    for f in (-2, -1):
+        ref[f] = (np.einsum("ic,it->ct", W[f].real, X[f].real)
+                  + 1j * np.einsum("ic,it->ct", W[f].imag, X[f].imag))
     assert rel_l2(Y, ref) < 2e-6
     assert rel_max(Y, ref) < 1e-5
 
