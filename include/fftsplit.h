@@ -101,8 +101,11 @@ typedef struct {
  *   weight spectra  W[bins][cin][cout_padded]        (wspec, wspec_bytes)
  *       = conj(DFT of w[co][ci] zero-padded top-left to L x L) / L^2,
  *         zero for co >= cout
- *   patch spectra   X[bins][cin][tiles_padded]       (workspace + xspec_offset)
- *   output spectra  Y[bins][cout_padded][tiles_padded] (workspace + yspec_offset)
+ *   patch spectra   X[cin16/16][bins][16][tiles_padded]  (workspace + xspec_offset)
+ *   output spectra  Y[cout_padded/16][bins][16][tiles_padded] (workspace + yspec_offset)
+ *       channel-blocked: channel c of bin f is row c % 16 of block c / 16
+ *       (cin16 = cin rounded up to a multiple of 16), so the slots of one
+ *       channel are 16 * tiles_padded elements apart
  * The DFT is unnormalised, exp(-2 pi i (m k1 + q k2) / L). */
 typedef struct {
     int tile;            /* T */

@@ -27,6 +27,9 @@ ERROR_INSUFFICIENT_WORKSPACE = 3
 ERROR_DEVICE = 4
 ERROR_ARCH = 5
 
+# patch and output spectra are stored in blocks of this many channels
+CHANNEL_BLOCK = 16
+
 OVERLAP_SAVE = 0
 OVERLAP_ADD = 1
 BIAS = 2
@@ -236,15 +239,22 @@ class Plan:
         return out
 
     # -- views of the workspace (complex64), for stage-level tests -------
-    def xspec_view(self, workspace):
+    def _unblock(self, raw, channels):
+        # channel-blocked [c/16][bins][c%16][tiles_padded] -> [bins][c][tiles_padded] (a copy)
         i = self.info
-        raw = workspace[i.xspec_offset:i.xspec_offset + i.xspec_bytes]
-        return raw.view(_torch().complex64).view(i.bins, self.cin, i.tiles_padded)
+        blocks = -(-channels // CHANNEL_BLOCK)
+        v = raw.view(_torch().complex64).view(blocks, i.bins, CHANNEL_BLOCK, i.tiles_padded)
+        return v.permute(1, 0, 2, 3).reshape(i.bins, blocks * CHANNEL_BLOCK, i.tiles_padded)[:, :channels]
+
+    def xspec_view(self, workspace):
+        """Patch spectra as [bins][cin][tiles_padded] (complex64, a copy)."""
+        i = self.info
+        return self._unblock(workspace[i.xspec_offset:i.xspec_offset + i.xspec_bytes], self.cin)
 
     def yspec_view(self, workspace):
+        """Output spectra as [bins][cout_padded][tiles_padded] (complex64, a copy)."""
         i = self.info
-        raw = workspace[i.yspec_offset:i.yspec_offset + i.yspec_bytes]
-        return raw.view(_torch().complex64).view(i.bins, i.cout_padded, i.tiles_padded)
+        return self._unblock(workspace[i.yspec_offset:i.yspec_offset + i.yspec_bytes], i.cout_padded)
 
     def wspec_view(self, wspec):
         i = self.info

@@ -56,6 +56,15 @@ constexpr int kBandNV8 = 8;
 constexpr int kBandNV16 = 8;
 constexpr int kBandNV32 = 16;
 
+// Patch and output spectra are channel-blocked (fftsplit.h):
+// [c / 16][bin][c % 16][patch], so the bins of one channel lie 16 * ntp
+// elements apart.  Element offset of (channel c, bin f, patch t):
+constexpr int kChanBlock = 16;
+__host__ __device__ inline size_t spec_offset(int c, int f, int t, int bins, int ntp) {
+    return ((size_t(c / kChanBlock) * bins + f) * kChanBlock + c % kChanBlock) * size_t(ntp) + t;
+}
+__host__ __device__ constexpr int round_up_block(int c) { return (c + kChanBlock - 1) / kChanBlock * kChanBlock; }
+
 // Stored frequency bins of an L x L real transform: L*L/2 (layout in
 // fftsplit.h).  Bins with k2 in [1, L/2-1] (all k1) are stored as they are;
 // of the columns k2 = 0 and k2 = L/2, which are Hermitian in k1, the

@@ -79,8 +79,13 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     const int t0 = tbk * BN;
 
     const float4* wsrc = reinterpret_cast<const float4*>(ws + size_t(f) * cin * coutp + co0);
-    const float4* xsrc = reinterpret_cast<const float4*>(xs + size_t(f) * cin * ntp + t0);
-    const int wrow4 = coutp / 2, xrow4 = ntp / 2;   // row pitch in float4
+    const int wrow4 = coutp / 2;   // row pitch in float4
+    // Patch spectra are channel-blocked (fftsplit.h): input channel ci of
+    // bin f starts at spec_offset(ci, f, 0); within a block of 16 channels
+    // the rows are ntp apart.
+    auto xrow = [&](int ci) {
+        return reinterpret_cast<const float4*>(xs + spec_offset(ci, f, t0, nbins, ntp));
+    };
 
     uint4 wreg[S::WL], xreg[S::XL];
     // A full stage is loaded as is; only a stage that runs past cin reads
@@ -98,7 +103,7 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
 #pragma unroll
             for (int i = 0; i < S::XL; ++i) {
                 const int e = i * S::NT + tid;
-                xreg[i] = reinterpret_cast<const uint4*>(xsrc)[(k0 + e / (BN / 2)) * xrow4 + e % (BN / 2)];
+                xreg[i] = reinterpret_cast<const uint4*>(xrow(k0 + e / (BN / 2)))[e % (BN / 2)];
             }
         } else {
 #pragma unroll
@@ -113,7 +118,7 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
             for (int i = 0; i < S::XL; ++i) {
                 const int e = i * S::NT + tid;
                 const int ci = k0 + e / (BN / 2);
-                const uint4 v = reinterpret_cast<const uint4*>(xsrc)[min(ci, cin - 1) * xrow4 + e % (BN / 2)];
+                const uint4 v = reinterpret_cast<const uint4*>(xrow(min(ci, cin - 1)))[e % (BN / 2)];
                 const unsigned m = ci < cin ? 0xffffffffu : 0u;
                 xreg[i] = make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
             }
@@ -211,17 +216,21 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-            float2* yb = ys + (size_t(f) * coutp + co0 + wm * (TM * 32) + i * 32) * ntp + t0 + wn * (TN * 32) +
-                         j * 32 + col;
+            // output spectra, channel-blocked: 32 channels = two blocks of 16
+            const int cb0 = co0 + wm * (TM * 32) + i * 32;
+            float2* yb = ys + spec_offset(cb0, f, t0 + wn * (TN * 32) + j * 32 + col, nbins, ntp);
+            const size_t blk = size_t(nbins) * kChanBlock * ntp;   // next block of 16 channels
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int ii = 8 * (r >> 2) + 4 * krow + (r & 3);
+                // row ii = 8 (r / 4) + 4 krow + r % 4 of the 32: block ii / 16 = r / 8
+                const int ii = 8 * ((r >> 2) & 1) + 4 * krow + (r & 3);
+                float2* dst = yb + size_t(ii) * ntp + (r >> 3) * blk;
                 if (G3) {
                     const float p1 = accR[i][j][r], p2 = accI[i][j][r];
-                    yb[size_t(ii) * ntp] = packed ? make_float2(p1, p2)
-                                                  : make_float2(p1 - p2, acc3[G3 ? i : 0][G3 ? j : 0][r] - p1 - p2);
+                    *dst = packed ? make_float2(p1, p2)
+                                  : make_float2(p1 - p2, acc3[G3 ? i : 0][G3 ? j : 0][r] - p1 - p2);
                 } else {
-                    yb[size_t(ii) * ntp] = make_float2(accR[i][j][r], accI[i][j][r]);
+                    *dst = make_float2(accR[i][j][r], accI[i][j][r]);
                 }
             }
         }

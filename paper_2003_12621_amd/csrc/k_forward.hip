@@ -18,8 +18,9 @@
 //   3. column pass: thread j >= 1 transforms column k2 = j; thread 0 the two
 //      real-valued columns k2 = 0 and k2 = L/2 packed as one complex
 //      sequence, then separates them;
-//   4. each bin goes to X[f][c][t]: the TG lanes with consecutive patch
-//      index write one contiguous 8*TG-byte segment.
+//   4. each bin goes to the patch spectra (channel-blocked, fftsplit.h):
+//      the TG lanes with consecutive patch index write one contiguous
+//      8*TG-byte segment.
 // Items are numbered channel-major (consecutive items are neighbouring
 // patch groups of one channel) and each accelerator die (XCD) receives a
 // contiguous range of workgroups, so the halo rows and columns shared by
@@ -64,8 +65,8 @@ __global__ __launch_bounds__(TG * (L / 2)) void forward_kernel(const float* __re
     const int q = lane % L;
     const int mr = lane / L;
     const unsigned row_step = unsigned(RPI * w * 4);
-    const BufRsrc rx = make_rsrc(xs, unsigned(size_t(cin) * ntp * 8 * stored_bins(L)));
-    const unsigned bs8 = unsigned(cin) * unsigned(ntp) * 8u;
+    const BufRsrc rx = make_rsrc(xs, unsigned(size_t(round_up_block(cin)) * ntp * 8 * stored_bins(L)));
+    const unsigned bs8 = unsigned(kChanBlock) * unsigned(ntp) * 8u;   // bin stride (channel-blocked)
 
     // Gather of one item into registers.  Wave wv reads the windows of its
     // own TPW patches; each wave-wide load covers RPI consecutive window
@@ -169,9 +170,9 @@ __global__ __launch_bounds__(TG * (L / 2)) void forward_kernel(const float* __re
             }
             __syncthreads();  // every read of the spectra is done before the next item's windows land
             fft<L, false>(cz);
-            // X[f][c][t0 + u]: per-lane byte offset, per-bin stride as the
+            // (c, f, t0 + u): per-lane byte offset, per-bin stride as the
             // scalar offset (always in range).
-            const unsigned voff = unsigned(c * ntp + t0 + u) * 8u;
+            const unsigned voff = unsigned(spec_offset(c, 0, t0 + u, stored_bins(L), ntp)) * 8u;
             if (j == 0) {
                 // the real bins (k1 = 0, L/2) of both columns share two slots
                 float2 a0, b0, ah, bh;
@@ -245,8 +246,8 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
     const int lrow = lane / w4;              // this lane's row within a load
     const int c4 = lane - lrow * w4;         // this lane's float4 column
     const BufRsrc rxin = make_rsrc(x, x_bytes);
-    const BufRsrc rx = make_rsrc(xs, unsigned(size_t(cin) * ntp * 8 * F));
-    const unsigned bs8 = unsigned(cin) * unsigned(ntp) * 8u;
+    const BufRsrc rx = make_rsrc(xs, unsigned(size_t(round_up_block(cin)) * ntp * 8 * F));
+    const unsigned bs8 = unsigned(kChanBlock) * unsigned(ntp) * 8u;   // bin stride (channel-blocked)
     // An opaque copy of a per-lane value: offsets derived from it are
     // recomputed inside the item loop instead of being hoisted out of it
     // and held in registers for the whole loop.
@@ -376,7 +377,7 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
         // and k2 = L/2 packed as one complex sequence (column 0 + i * column
         // L/2).  Both kinds of lane run one instruction stream -- packing and
         // separating the two real spectra are selects -- so no wave executes
-        // two paths.  Each bin goes to X[f][c][t0 + u]: the TG lanes of
+        // two paths.  Each bin goes to (c, f, t0 + u): the TG lanes of
         // consecutive patches write one contiguous 8*TG-byte segment.
         {
             const int u = tid % TG;
@@ -397,7 +398,7 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
             // Lane j >= 1 stores bins (k1, j) and (k1 + L/2, j); lane 0 the
             // complex bins k1 in [1, L/2-1] of the two real columns, and at
             // k1 = 0 their four real bins packed into two slots.
-            const unsigned lane8 = unsigned(c * ntp + t0 + u) * 8u;
+            const unsigned lane8 = unsigned(spec_offset(c, 0, t0 + u, F, ntp)) * 8u;
             const unsigned va0 = lane8 + unsigned(j0 ? bin_real_a(L) : bin_mid(L, 0, j)) * bs8;
             const unsigned vb0 = lane8 + unsigned(j0 ? bin_real_b(L) : bin_mid(L, H2, j)) * bs8;
             const unsigned va = lane8 + unsigned(j0 ? bin_col0(L, 1) - 1 : bin_mid(L, 0, j)) * bs8;

@@ -88,14 +88,14 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
         cols_ok[tid] = cw;
     }
 
-    // 1. column pass: Y[f][co][t0 + u] with a per-lane byte offset and the
-    // per-bin stride as the scalar offset (always in range).
+    // 1. column pass: output spectra (co, f, t0 + u) with a per-lane byte
+    // offset and the per-bin stride as the scalar offset (always in range).
     {
         const int u = tid % TG;
         const int j = tid / TG;
         const BufRsrc ry = make_rsrc(ys, unsigned(size_t(coutp) * ntp * 8 * stored_bins(L)));
-        const unsigned bs8 = unsigned(coutp) * unsigned(ntp) * 8u;
-        const unsigned voff = unsigned(co * ntp + t0 + u) * 8u;
+        const unsigned bs8 = unsigned(kChanBlock) * unsigned(ntp) * 8u;   // bin stride (channel-blocked)
+        const unsigned voff = unsigned(spec_offset(co, 0, t0 + u, stored_bins(L), ntp)) * 8u;
         float2 cz[L];
         if (j == 0) {
             float2 y0[H2 + 1], yh[H2 + 1];
@@ -287,7 +287,7 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const BufRsrc ry = make_rsrc(ys, unsigned(size_t(coutp) * ntp * 8 * F));
     const BufRsrc ryo = make_rsrc(y, y_bytes);
-    const unsigned bs8 = unsigned(coutp) * unsigned(ntp) * 8u;
+    const unsigned bs8 = unsigned(kChanBlock) * unsigned(ntp) * 8u;   // bin stride (channel-blocked)
     auto opaque = [](int v) {
         asm volatile("" : "+v"(v));
         return v;
@@ -315,7 +315,7 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
             t0 = (item - co * ngroups) * TG;
             ok = true;
         }
-        const unsigned lane8 = unsigned(co * ntp + t0 + opaque(uc)) * 8u;
+        const unsigned lane8 = unsigned(spec_offset(co, 0, t0 + opaque(uc), F, ntp)) * 8u;
         const unsigned va0 = ok ? lane8 + unsigned(j0 ? bin_real_a(L) : bin_mid(L, 0, jc)) * bs8 : kOutOfRange;
         const unsigned vb0 = ok ? lane8 + unsigned(j0 ? bin_real_b(L) : bin_mid(L, H2, jc)) * bs8 : kOutOfRange;
         const unsigned va = ok ? lane8 + unsigned(j0 ? bin_col0(L, 1) - 1 : bin_mid(L, 0, jc)) * bs8 : kOutOfRange;

@@ -208,7 +208,7 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
 
     // Byte sizes with overflow checks.
     size_t xs, ys, wsb, tmp;
-    if (!mul_ok(size_t(g.bins) * 8, size_t(p.cin), &tmp) || !mul_ok(tmp, size_t(g.ntp), &xs) ||
+    if (!mul_ok(size_t(g.bins) * 8, size_t(round_up_block(p.cin)), &tmp) || !mul_ok(tmp, size_t(g.ntp), &xs) ||
         !mul_ok(size_t(g.bins) * 8, size_t(g.coutp), &tmp) || !mul_ok(tmp, size_t(g.ntp), &ys) ||
         !mul_ok(size_t(g.bins) * 8, size_t(p.cin), &tmp) || !mul_ok(tmp, size_t(g.coutp), &wsb))
         return fail(FFTSPLIT_ERROR_INVALID_VALUE, "buffer sizes overflow size_t");

@@ -51,7 +51,7 @@ def test_first_config_geometry():
     assert i.tiles_padded % 64 == 0 and i.tiles_padded >= 36
     assert i.cout_padded >= 16
     assert i.wspec_bytes == 8 * i.bins * 3 * i.cout_padded
-    assert i.xspec_bytes == 8 * i.bins * 3 * i.tiles_padded
+    assert i.xspec_bytes == 8 * i.bins * 16 * i.tiles_padded   # channels in blocks of 16
     assert i.yspec_bytes == 8 * i.bins * i.cout_padded * i.tiles_padded
     assert i.yspec_offset >= i.xspec_offset + i.xspec_bytes
     assert i.workspace_bytes >= i.yspec_offset + i.yspec_bytes
