@@ -63,9 +63,11 @@ def build(verbose: bool = False) -> str:
 
 # Sources each timed kernel is compiled from (for profile-record validity).
 KERNEL_SOURCES = {
-    "forward": ["k_forward.hip", "fft_regs.hpp", "twiddles.inc", "launch_util.hpp", "fftsplit_internal.hpp"],
+    "forward": ["k_forward.hip", "band.hpp", "fft_regs.hpp", "twiddles.inc", "launch_util.hpp",
+                "fftsplit_internal.hpp"],
     "contract": ["k_contract.hip", "launch_util.hpp", "fftsplit_internal.hpp"],
-    "inverse": ["k_inverse.hip", "fft_regs.hpp", "twiddles.inc", "launch_util.hpp", "fftsplit_internal.hpp"],
+    "inverse": ["k_inverse.hip", "band.hpp", "fft_regs.hpp", "twiddles.inc", "launch_util.hpp",
+                "fftsplit_internal.hpp"],
 }
 
 
