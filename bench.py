@@ -125,6 +125,9 @@ def bench_vgg16(args):
     s = 224
     for i, (cin, cout, hw) in enumerate(VGG16_LAYERS, start=1):
         flops += 2 * VGG_BATCH * cout * hw * hw * cin * 9
+    spatial = None
+    if not args.no_compare:
+        spatial = time_vgg_spatial(args, layers, x, stack)
     out = {"metric": "effective direct-conv GFLOP/s", "value": round(flops / (ms * 1e-3) / 1e9, 1),
            "unit": "GFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
            "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
@@ -132,7 +135,57 @@ def bench_vgg16(args):
            "config": {"workload": f"vgg16 conv stack, batch {VGG_BATCH}, 3x224x224, bias+ReLU, 5 max-pools",
                       "tiles": stack.tiles, "mode": args.mode},
            "images_per_s": round(VGG_BATCH / (ms * 1e-3), 1)}
+    if spatial is not None:
+        for v in spatial.values():
+            if isinstance(v, dict):
+                v["GFLOP/s"] = round(flops / (v["ms"] * 1e-3) / 1e9, 1)
+        out["spatial_methods"] = spatial
     print(json.dumps(out), flush=True)
+
+
+def time_vgg_spatial(args, layers, x, split_stack):
+    """The VGG-16 stack by spatial convolution: this library's direct kernel
+    (the same stack object, method="direct") and torch's fp32 conv2d +
+    max_pool2d (MIOpen).  Returns {name: {"ms": ...}} per forward."""
+    import torch
+    import torch.nn.functional as F
+    from paper_2003_12621_amd.vgg import POOL_AFTER, VGG16Stack
+    from workloads import VGG_BATCH
+
+    torch.backends.cudnn.allow_tf32 = False
+    dev = split_stack.device
+    xd = torch.from_numpy(x).to(dev)
+    direct = VGG16Stack(layers, batch=VGG_BATCH, method="direct")
+    tw = [(torch.from_numpy(w).to(dev), torch.from_numpy(b).to(dev)) for w, b in layers]
+
+    def torch_stack():
+        a = xd
+        for i, (w, b) in enumerate(tw, start=1):
+            a = F.relu(F.conv2d(a, w, b, padding=1))
+            if i in POOL_AFTER:
+                a = F.max_pool2d(a, 2)
+        return a
+
+    res = {}
+    for name, fn in (("direct_hip", lambda: direct.forward(xd)), ("torch_conv2d", torch_stack)):
+        for _ in range(max(args.warmup, 2)):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        res[name] = {"ms": round(e0.elapsed_time(e1) / args.steps, 4)}
+    ys = split_stack.forward(xd).clone()
+    yd = direct.forward(xd).clone()
+    yt = torch_stack()
+    torch.cuda.synchronize()
+    nt = torch.linalg.vector_norm(yt)
+    res["direct_hip"]["rel_l2_vs_torch"] = float(torch.linalg.vector_norm(yd - yt) / nt)
+    res["split_rel_l2_vs_torch"] = float(torch.linalg.vector_norm(ys - yt) / nt)
+    return res
 
 
 def main():
@@ -145,6 +198,8 @@ def main():
     ap.add_argument("--mode", default="os", choices=["os", "oaa"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true")
+    ap.add_argument("--no-compare", action="store_true",
+                    help="skip timing the spatial methods (this library's direct kernel, torch/MIOpen conv2d)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="before timing, copy a buffer of this many MiB 3 times (calibrates HBM counters)")
     args = ap.parse_args()
@@ -285,9 +340,43 @@ def main():
         "wall_s_timed": round(t_wall, 4),
         "parity_rel_l2": parity,
     }
+    if not args.no_compare:
+        out["spatial_methods"] = time_spatial_methods(args, plan, layer, xd, wd, bd)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layer, x, w, b, tile)
     print(json.dumps(out), flush=True)
+
+
+def time_spatial_methods(args, plan, layer, xd, wd, bd):
+    """The same layer by spatial convolution, timed the same way (context for
+    the split method's speed, as the paper sets it beside direct convolution):
+    this library's direct kernel (fftsplit_direct_conv2d) and torch's fp32
+    conv2d (MIOpen), both on torch's current stream."""
+    import torch
+    import torch.nn.functional as F
+
+    torch.backends.cudnn.allow_tf32 = False
+    wdir = plan.direct_transform_weights(wd)
+    yd = plan.new_output()
+    res = {}
+    runs = {"direct_hip": lambda: plan.direct_conv2d(xd, wdir, bd, out=yd),
+            "torch_conv2d": lambda: F.conv2d(xd, wd, bd, padding=layer.k // 2)}
+    for name, fn in runs.items():
+        for _ in range(max(args.warmup, 2)):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        res[name] = {"ms": round(ms, 4), "GFLOP/s": round(layer.direct_flops / (ms * 1e-3) / 1e9, 1)}
+    yt = F.conv2d(xd, wd, bd, padding=layer.k // 2)
+    torch.cuda.synchronize()
+    res["direct_hip"]["rel_l2_vs_torch"] = float(torch.linalg.vector_norm(yd - yt) / torch.linalg.vector_norm(yt))
+    return res
 
 
 if __name__ == "__main__":

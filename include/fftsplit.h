@@ -127,6 +127,9 @@ typedef struct {
      * per complex multiply-add.  The environment variable
      * FFTSPLIT_CONTRACT_TILE=[g3:|g4:]MxNxK overrides it at plan time. */
     int contract_tile_m, contract_tile_n, contract_stage_k, contract_real_products;
+    /* Bytes of the filter layout of the direct (spatial) convolution,
+     * fftsplit_direct_transform_weights. */
+    size_t direct_wspec_bytes;
 } fftsplit_plan_info_t;
 
 /* Validate `prob` (host) and create a plan for `device` (a HIP ordinal).
@@ -177,6 +180,24 @@ fftsplit_status_t fftsplit_contract(fftsplit_plan_t plan, const void* wspec, voi
                                     size_t workspace_bytes, hipStream_t stream);
 fftsplit_status_t fftsplit_inverse(fftsplit_plan_t plan, const float* bias, float* y,
                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* The spatial convolution the paper compares the split method against
+ * (Section 2, eq. 1 computed directly; Section 4): the same layer as the
+ * plan's, as an implicit matrix product on the fp32 matrix cores, with the
+ * plan's bias and ReLU flags.  The filters are first rearranged once per
+ * layer:
+ *   fftsplit_direct_transform_weights: w (device) [cout][cin][k][k] ->
+ *     wd (device, info.direct_wspec_bytes) = [k*k][cin16][cout_padded],
+ *     zero for padded channels;
+ *   fftsplit_direct_conv2d: x (device) [n][cin][h][w], wd, bias (device,
+ *     [cout] or NULL; required iff FFTSPLIT_BIAS), y (device)
+ *     [n][cout][h][w] (must not overlap x or wd).  No workspace.  x must be
+ *     under 2 GiB (FFTSPLIT_ERROR_NOT_SUPPORTED otherwise).
+ * The plan's tile size and overlap mode do not apply. */
+fftsplit_status_t fftsplit_direct_transform_weights(fftsplit_plan_t plan, const float* w, float* wd,
+                                                    hipStream_t stream);
+fftsplit_status_t fftsplit_direct_conv2d(fftsplit_plan_t plan, const float* x, const float* wd, const float* bias,
+                                         float* y, hipStream_t stream);
 
 /* 2x2, stride-2 max-pool (floor), used between the stages of a VGG-16
  * stack; not part of the method.  x (device) [n][c][h][w] ->

@@ -51,7 +51,8 @@ class PlanInfo(ctypes.Structure):
                 ("yspec_offset", ctypes.c_size_t), ("yspec_bytes", ctypes.c_size_t),
                 ("aux_offset", ctypes.c_size_t), ("aux_bytes", ctypes.c_size_t),
                 ("contract_tile_m", ctypes.c_int), ("contract_tile_n", ctypes.c_int),
-                ("contract_stage_k", ctypes.c_int), ("contract_real_products", ctypes.c_int)]
+                ("contract_stage_k", ctypes.c_int), ("contract_real_products", ctypes.c_int),
+                ("direct_wspec_bytes", ctypes.c_size_t)]
 
 
 class FftsplitError(RuntimeError):
@@ -81,6 +82,10 @@ _SIGNATURES = {
                                         ctypes.c_size_t, ctypes.c_void_p]),
     "fftsplit_maxpool2x2": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
                                            ctypes.c_int, ctypes.c_int, ctypes.c_void_p]),
+    "fftsplit_direct_transform_weights": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                                         ctypes.c_void_p]),
+    "fftsplit_direct_conv2d": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_void_p, ctypes.c_void_p]),
     "fftsplit_set_timing_events": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
     "fftsplit_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "fftsplit_last_error": (ctypes.c_char_p, []),
@@ -236,6 +241,30 @@ class Plan:
         _check(lib().fftsplit_inverse(self._h, bp, yp, _dev_tensor(workspace, "workspace"),
                                       workspace.numel() * workspace.element_size(), _stream_handle(self.device)),
                "fftsplit_inverse")
+        return out
+
+    # -- the spatial (direct) convolution of the same layer --------------
+    def direct_transform_weights(self, w, out=None):
+        """Filters rearranged for fftsplit_direct_conv2d, once per layer."""
+        torch = _torch()
+        wp = _dev_tensor(w, "w", torch.float32, self.cout * self.cin * self.k * self.k)
+        if out is None:
+            out = torch.empty(self.info.direct_wspec_bytes // 4, dtype=torch.float32, device=self.device)
+        if out.numel() * out.element_size() < self.info.direct_wspec_bytes:
+            raise ValueError("direct weight buffer too small")
+        _check(lib().fftsplit_direct_transform_weights(self._h, wp, _dev_tensor(out, "wd"),
+                                                       _stream_handle(self.device)),
+               "fftsplit_direct_transform_weights")
+        return out
+
+    def direct_conv2d(self, x, wd, bias=None, out=None):
+        torch = _torch()
+        xp = _dev_tensor(x, "x", torch.float32, self.n * self.cin * self.h * self.w)
+        out = self.new_output() if out is None else out
+        yp = _dev_tensor(out, "y", torch.float32, self.n * self.cout * self.h * self.w)
+        bp = None if bias is None else _dev_tensor(bias, "bias", torch.float32, self.cout)
+        _check(lib().fftsplit_direct_conv2d(self._h, xp, _dev_tensor(wd, "wd"), bp, yp,
+                                            _stream_handle(self.device)), "fftsplit_direct_conv2d")
         return out
 
     # -- views of the workspace (complex64), for stage-level tests -------

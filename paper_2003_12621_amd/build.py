@@ -16,7 +16,8 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libfftsplit.so")
 
-SOURCES = ["plan.cpp", "api.cpp", "k_weights.hip", "k_forward.hip", "k_contract.hip", "k_inverse.hip", "k_pool.hip"]
+SOURCES = ["plan.cpp", "api.cpp", "k_weights.hip", "k_forward.hip", "k_contract.hip", "k_inverse.hip", "k_pool.hip",
+           "k_direct.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

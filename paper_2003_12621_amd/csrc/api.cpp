@@ -180,6 +180,37 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_maxpool2x2(const float* x, float* y, 
     return launched(launch_maxpool(x, y, n, c, h, w, stream), "max-pool launch");
 }
 
+FFTSPLIT_EXPORT fftsplit_status_t fftsplit_direct_transform_weights(fftsplit_plan_t plan, const float* w, float* wd,
+                                                                    hipStream_t stream) {
+    set_error("");
+    if (fftsplit_status_t s = check_plan(plan)) return s;
+    if (fftsplit_status_t s = check_ptr(w, "w")) return s;
+    if (fftsplit_status_t s = check_ptr(wd, "wd")) return s;
+    const size_t wb = size_t(plan->prob.cout) * plan->prob.cin * plan->prob.k * plan->prob.k * 4;
+    if (overlap(w, wb, wd, direct_wspec_bytes(*plan))) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "w overlaps wd");
+    DeviceGuard g(plan->device);
+    if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
+    return launched(launch_direct_weights(*plan, w, wd, stream), "direct weight layout launch");
+}
+
+FFTSPLIT_EXPORT fftsplit_status_t fftsplit_direct_conv2d(fftsplit_plan_t plan, const float* x, const float* wd,
+                                                         const float* bias, float* y, hipStream_t stream) {
+    set_error("");
+    if (fftsplit_status_t s = check_plan(plan)) return s;
+    if (fftsplit_status_t s = check_ptr(x, "x")) return s;
+    if (fftsplit_status_t s = check_ptr(wd, "wd")) return s;
+    if (fftsplit_status_t s = check_ptr(y, "y")) return s;
+    if (fftsplit_status_t s = check_bias(plan, bias)) return s;
+    if (overlap(x, x_bytes(plan), y, y_bytes(plan))) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "y overlaps x");
+    if (overlap(wd, direct_wspec_bytes(*plan), y, y_bytes(plan)))
+        return fail(FFTSPLIT_ERROR_INVALID_VALUE, "y overlaps wd");
+    if (x_bytes(plan) > 0x7fffffffu)
+        return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "direct convolution: the input must be under 2 GiB");
+    DeviceGuard g(plan->device);
+    if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
+    return launched(launch_direct(*plan, x, wd, bias, y, stream, t_events), "direct convolution launch");
+}
+
 FFTSPLIT_EXPORT fftsplit_status_t fftsplit_set_timing_events(hipEvent_t start, hipEvent_t stop) {
     set_error("");
     t_events.start = start;

@@ -96,5 +96,9 @@ hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xspec, const 
 hipError_t launch_inverse(const fftsplit_plan_s& p, const float2* yspec, const float* bias, float* y, void* aux,
                           hipStream_t s, const LaunchEvents& ev);
 hipError_t launch_maxpool(const float* x, float* y, int n, int c, int h, int w, hipStream_t s);
+size_t direct_wspec_bytes(const fftsplit_plan_s& p);
+hipError_t launch_direct_weights(const fftsplit_plan_s& p, const float* w, float* wd, hipStream_t s);
+hipError_t launch_direct(const fftsplit_plan_s& p, const float* x, const float* wd, const float* bias, float* y,
+                         hipStream_t s, const LaunchEvents& ev);
 
 }  // namespace fftsplit

@@ -356,6 +356,7 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_plan_info(fftsplit_plan_t plan, fftsp
     i.contract_tile_n = plan->con_bn;
     i.contract_stage_k = plan->con_kc;
     i.contract_real_products = plan->con_products;
+    i.direct_wspec_bytes = direct_wspec_bytes(*plan);
     *out = i;
     return FFTSPLIT_SUCCESS;
 }

@@ -7,6 +7,10 @@ all through the library's C ABI: each layer has its own plan (tile size
 chosen by the plan unless given) and filter spectra, transformed once at
 construction; one workspace (the largest any layer needs) and two
 activation buffers are shared by all layers.
+
+With method="direct" the same stack runs on the library's spatial
+convolution (fftsplit_direct_conv2d), the method the paper compares
+against on these layers; the plans then serve only as layer descriptors.
 """
 from __future__ import annotations
 
@@ -19,12 +23,15 @@ POOL_AFTER = (2, 4, 7, 10, 13)
 
 class VGG16Stack:
     def __init__(self, layers: Sequence, batch: int, hw: int = 224, tiles: Optional[Sequence[int]] = None,
-                 mode: str = "os", device=None):
+                 mode: str = "os", device=None, method: str = "split"):
         """`layers`: 13 (w, b) pairs (torch CUDA float32 tensors or arrays);
         `tiles`: optional per-layer tile sizes (0 or None = plan's choice)."""
         import torch
         if len(layers) != 13:
             raise ValueError("VGG-16 has 13 convolution layers")
+        if method not in ("split", "direct"):
+            raise ValueError("method must be 'split' or 'direct'")
+        self.method = method
         dev = torch.device("cuda", torch.cuda.current_device() if device is None else int(device))
         self.device = dev
         self.batch = batch
@@ -40,13 +47,13 @@ class VGG16Stack:
             t = 0 if tiles is None or not tiles[i - 1] else int(tiles[i - 1])
             plan = Plan(batch, cin, s, s, cout, k, tile=t, mode=mode, bias=True, relu=True, device=dev.index)
             self.plans.append(plan)
-            self.wspecs.append(plan.transform_weights(w))
+            self.wspecs.append(plan.transform_weights(w) if method == "split" else plan.direct_transform_weights(w))
             self.biases.append(b)
             shapes.append((batch, cout, s, s))
             if i in POOL_AFTER:
                 s //= 2
-        self.workspace = torch.empty(max(p.info.workspace_bytes for p in self.plans), dtype=torch.uint8,
-                                     device=dev)
+        self.workspace = (torch.empty(max(p.info.workspace_bytes for p in self.plans), dtype=torch.uint8,
+                                      device=dev) if method == "split" else None)
         biggest = max(max(n * c * h * w for n, c, h, w in shapes), batch * 3 * hw * hw)
         self._buf = [torch.empty(biggest, dtype=torch.float32, device=dev) for _ in range(2)]
 
@@ -65,7 +72,10 @@ class VGG16Stack:
         for i, plan in enumerate(self.plans, start=1):
             shape = (plan.n, plan.cout, plan.h, plan.w)
             y = other[: plan.n * plan.cout * plan.h * plan.w].view(shape)
-            plan.conv2d(a, self.wspecs[i - 1], self.biases[i - 1], out=y, workspace=self.workspace)
+            if self.method == "split":
+                plan.conv2d(a, self.wspecs[i - 1], self.biases[i - 1], out=y, workspace=self.workspace)
+            else:
+                plan.direct_conv2d(a, self.wspecs[i - 1], self.biases[i - 1], out=y)
             if keep:
                 outs.append(y.clone())
             if i in POOL_AFTER:

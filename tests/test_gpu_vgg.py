@@ -36,9 +36,15 @@ def vgg_run():
     return x, layers, got, final, POOL_AFTER
 
 
-def test_vgg16_chain_matches_oracle(vgg_run):
+@pytest.fixture(scope="module")
+def vgg_ref():
+    x, layers = make_vgg16(batch=32, seed=0)
+    return oracle.vgg16_forward(x[SAMPLE], layers, return_all=True)
+
+
+def test_vgg16_chain_matches_oracle(vgg_run, vgg_ref):
     x, layers, got, final, _ = vgg_run
-    ref_outs, ref_final = oracle.vgg16_forward(x[SAMPLE], layers, return_all=True)
+    ref_outs, ref_final = vgg_ref
     assert final.shape == (2, 512, 7, 7)
     for i, (g, r) in enumerate(zip(got, ref_outs), start=1):
         err = rel_l2(g, r)
@@ -57,3 +63,17 @@ def test_vgg16_each_layer_on_gpu_input(vgg_run):
         a = got[i - 1].astype(np.float64)
         if i in pool_after:
             a = oracle.maxpool2x2(a)
+
+
+def test_vgg16_direct_stack_matches_oracle(vgg_ref):
+    """The same stack on the spatial convolution (method="direct"), on a
+    batch of 2: final activation against the float64 chain."""
+    from paper_2003_12621_amd.vgg import VGG16Stack
+    x, layers = make_vgg16(batch=32, seed=0)
+    xs = np.ascontiguousarray(x[SAMPLE])
+    stack = VGG16Stack(layers, batch=len(SAMPLE), method="direct")
+    out = stack.forward(torch.from_numpy(xs).cuda())
+    torch.cuda.synchronize()
+    err = rel_l2(out.cpu().numpy(), vgg_ref[1])
+    print(f"[vgg] direct stack final rel_l2 = {err:.3e}", flush=True)
+    assert err <= 1e-4
