@@ -102,10 +102,13 @@ typedef struct {
  *       = conj(DFT of w[co][ci] zero-padded top-left to L x L) / L^2,
  *         zero for co >= cout
  *   patch spectra   X[cin16/16][bins][16][tiles_padded]  (workspace + xspec_offset)
- *   output spectra  Y[cout_padded/16][bins][16][tiles_padded] (workspace + yspec_offset)
  *       channel-blocked: channel c of bin f is row c % 16 of block c / 16
  *       (cin16 = cin rounded up to a multiple of 16), so the slots of one
  *       channel are 16 * tiles_padded elements apart
+ *   output spectra  Y[cout_padded][tiles_padded/G][bins][G] (workspace + yspec_offset)
+ *       patch-group-major, G = spec_group (64, 32, 16 for L = 8, 16, 32):
+ *       all slots of one channel and G consecutive patches are one
+ *       contiguous run (the unit of work of the inverse transform)
  * The DFT is unnormalised, exp(-2 pi i (m k1 + q k2) / L). */
 typedef struct {
     int tile;            /* T */
@@ -127,6 +130,7 @@ typedef struct {
      * per complex multiply-add.  The environment variable
      * FFTSPLIT_CONTRACT_TILE=[g3:|g4:]MxNxK overrides it at plan time. */
     int contract_tile_m, contract_tile_n, contract_stage_k, contract_real_products;
+    int spec_group;      /* G of the output-spectra layout */
     /* Bytes of the filter layout of the direct (spatial) convolution,
      * fftsplit_direct_transform_weights. */
     size_t direct_wspec_bytes;

@@ -52,7 +52,7 @@ class PlanInfo(ctypes.Structure):
                 ("aux_offset", ctypes.c_size_t), ("aux_bytes", ctypes.c_size_t),
                 ("contract_tile_m", ctypes.c_int), ("contract_tile_n", ctypes.c_int),
                 ("contract_stage_k", ctypes.c_int), ("contract_real_products", ctypes.c_int),
-                ("direct_wspec_bytes", ctypes.c_size_t)]
+                ("spec_group", ctypes.c_int), ("direct_wspec_bytes", ctypes.c_size_t)]
 
 
 class FftsplitError(RuntimeError):
@@ -283,7 +283,10 @@ class Plan:
     def yspec_view(self, workspace):
         """Output spectra as [bins][cout_padded][tiles_padded] (complex64, a copy)."""
         i = self.info
-        return self._unblock(workspace[i.yspec_offset:i.yspec_offset + i.yspec_bytes], i.cout_padded)
+        g = i.spec_group
+        raw = workspace[i.yspec_offset:i.yspec_offset + i.yspec_bytes]
+        v = raw.view(_torch().complex64).view(i.cout_padded, i.tiles_padded // g, i.bins, g)
+        return v.permute(2, 0, 1, 3).reshape(i.bins, i.cout_padded, i.tiles_padded)
 
     def wspec_view(self, wspec):
         i = self.info

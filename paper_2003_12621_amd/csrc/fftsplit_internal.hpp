@@ -65,6 +65,15 @@ __host__ __device__ inline size_t spec_offset(int c, int f, int t, int bins, int
 }
 __host__ __device__ constexpr int round_up_block(int c) { return (c + kChanBlock - 1) / kChanBlock * kChanBlock; }
 
+// Output spectra are patch-group-major (fftsplit.h): [c][t / G][bin][t % G]
+// with G = patch_group(L), so one inverse work item (channel c, patches
+// [gG, gG + G)) reads one contiguous run of bins * G elements.  The
+// contraction, which is bound by its matrix products, writes them as
+// G-element runs instead.  Element offset of (channel c, bin f, patch t):
+__host__ __device__ inline size_t yspec_offset(int c, int f, int t, int bins, int G, int ngroups) {
+    return ((size_t(c) * ngroups + t / G) * bins + f) * size_t(G) + t % G;
+}
+
 // Stored frequency bins of an L x L real transform: L*L/2 (layout in
 // fftsplit.h).  Bins with k2 in [1, L/2-1] (all k1) are stored as they are;
 // of the columns k2 = 0 and k2 = L/2, which are Hermitian in k1, the

@@ -27,7 +27,9 @@
 // stage s+1 is loaded from memory into registers while stage s is
 // multiplied out of LDS, then written to the other LDS buffer (one barrier
 // per stage).  Inside a stage the operand fragments of the next channel
-// pair are read from LDS while the current pair's MFMAs run.  The channel
+// pair are read from LDS while the current pair's MFMAs run.  The filter
+// spectra, the bulk of the bytes and each read once, are loaded
+// non-temporally so they do not evict the patch and output spectra.  The channel
 // blocks of one bin are consecutive logical workgroups on the same XCD, so
 // the bin's patch spectra are fetched from HBM once and reused from L2.
 #include "fftsplit_internal.hpp"
@@ -56,7 +58,7 @@ struct ConShape {
 template <int BM, int BN, int KC, int WM, bool G3>
 __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict__ xs, const float2* __restrict__ ws,
                                                        float2* __restrict__ ys, int cin, int coutp, int ntp,
-                                                       int nbco, int nbt, int nbins) {
+                                                       int nbco, int nbt, int nbins, int ygroup) {
     using S = ConShape<BM, BN, KC, WM>;
     constexpr int TM = S::TM, TN = S::TN;
     extern __shared__ float4 lds_raw[];
@@ -98,7 +100,8 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
 #pragma unroll
             for (int i = 0; i < S::WL; ++i) {
                 const int e = i * S::NT + tid;
-                wreg[i] = reinterpret_cast<const uint4*>(wsrc)[(k0 + e / (BM / 2)) * wrow4 + e % (BM / 2)];
+                wreg[i] = load_stream_u4(reinterpret_cast<const uint4*>(wsrc) + (k0 + e / (BM / 2)) * wrow4 +
+                                         e % (BM / 2));
             }
 #pragma unroll
             for (int i = 0; i < S::XL; ++i) {
@@ -110,7 +113,8 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
             for (int i = 0; i < S::WL; ++i) {
                 const int e = i * S::NT + tid;
                 const int ci = k0 + e / (BM / 2);
-                const uint4 v = reinterpret_cast<const uint4*>(wsrc)[min(ci, cin - 1) * wrow4 + e % (BM / 2)];
+                const uint4 v = load_stream_u4(reinterpret_cast<const uint4*>(wsrc) + min(ci, cin - 1) * wrow4 +
+                                               e % (BM / 2));
                 const unsigned m = ci < cin ? 0xffffffffu : 0u;
                 wreg[i] = make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
             }
@@ -216,15 +220,17 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-            // output spectra, channel-blocked: 32 channels = two blocks of 16
+            // output spectra, patch-group-major: the 32 lanes of a row write
+            // 32 consecutive patches (32 / G runs of G, or half a run)
             const int cb0 = co0 + wm * (TM * 32) + i * 32;
-            float2* yb = ys + spec_offset(cb0, f, t0 + wn * (TN * 32) + j * 32 + col, nbins, ntp);
-            const size_t blk = size_t(nbins) * kChanBlock * ntp;   // next block of 16 channels
+            float2* yb = ys + yspec_offset(cb0, f, t0 + wn * (TN * 32) + j * 32 + col, nbins, ygroup,
+                                           ntp / ygroup);
+            const size_t cstride = size_t(nbins) * ntp;   // next channel
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                // row ii = 8 (r / 4) + 4 krow + r % 4 of the 32: block ii / 16 = r / 8
-                const int ii = 8 * ((r >> 2) & 1) + 4 * krow + (r & 3);
-                float2* dst = yb + size_t(ii) * ntp + (r >> 3) * blk;
+                // row ii = 8 (r / 4) + 4 krow + r % 4 of the 32
+                const int ii = 8 * (r >> 2) + 4 * krow + (r & 3);
+                float2* dst = yb + size_t(ii) * cstride;
                 if (G3) {
                     const float p1 = accR[i][j][r], p2 = accI[i][j][r];
                     *dst = packed ? make_float2(p1, p2)
@@ -248,7 +254,7 @@ static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, 
     const int nbco = p.coutp / BM, nbt = p.ntp / BN;
     const size_t nb = size_t(nbco) * nbt * p.bins;
     return launch_kernel(kern, dim3(unsigned(nb)), dim3(S::NT), S::LDS_BYTES, s, ev.start, ev.stop, xs, ws, ys,
-                         p.prob.cin, p.coutp, p.ntp, nbco, nbt, p.bins);
+                         p.prob.cin, p.coutp, p.ntp, nbco, nbt, p.bins, patch_group(p.L));
 }
 
 hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xs, const float2* ws, float2* ys,

@@ -94,8 +94,9 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
         const int u = tid % TG;
         const int j = tid / TG;
         const BufRsrc ry = make_rsrc(ys, unsigned(size_t(coutp) * ntp * 8 * stored_bins(L)));
-        const unsigned bs8 = unsigned(kChanBlock) * unsigned(ntp) * 8u;   // bin stride (channel-blocked)
-        const unsigned voff = unsigned(spec_offset(co, 0, t0 + u, stored_bins(L), ntp)) * 8u;
+        static_assert(TG == patch_group(L), "a work item is one patch group of the output spectra");
+        const unsigned bs8 = unsigned(TG) * 8u;   // bin stride (patch-group-major)
+        const unsigned voff = unsigned(yspec_offset(co, 0, t0 + u, stored_bins(L), TG, ngroups)) * 8u;
         float2 cz[L];
         if (j == 0) {
             float2 y0[H2 + 1], yh[H2 + 1];
@@ -287,7 +288,8 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const BufRsrc ry = make_rsrc(ys, unsigned(size_t(coutp) * ntp * 8 * F));
     const BufRsrc ryo = make_rsrc(y, y_bytes);
-    const unsigned bs8 = unsigned(kChanBlock) * unsigned(ntp) * 8u;   // bin stride (channel-blocked)
+    static_assert(TG == patch_group(L), "a work item is one patch group of the output spectra");
+    const unsigned bs8 = unsigned(TG) * 8u;   // bin stride (patch-group-major)
     auto opaque = [](int v) {
         asm volatile("" : "+v"(v));
         return v;
@@ -315,7 +317,8 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
             t0 = (item - co * ngroups) * TG;
             ok = true;
         }
-        const unsigned lane8 = unsigned(spec_offset(co, 0, t0 + opaque(uc), F, ntp)) * 8u;
+        // item = co * ngroups + t0 / TG: the item's run starts at item * F * TG
+        const unsigned lane8 = unsigned(yspec_offset(co, 0, t0 + opaque(uc), F, TG, ngroups)) * 8u;
         const unsigned va0 = ok ? lane8 + unsigned(j0 ? bin_real_a(L) : bin_mid(L, 0, jc)) * bs8 : kOutOfRange;
         const unsigned vb0 = ok ? lane8 + unsigned(j0 ? bin_real_b(L) : bin_mid(L, H2, jc)) * bs8 : kOutOfRange;
         const unsigned va = ok ? lane8 + unsigned(j0 ? bin_col0(L, 1) - 1 : bin_mid(L, 0, jc)) * bs8 : kOutOfRange;
@@ -346,9 +349,12 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
 
         // column pass
         {
-            // lane 0: column spectra Y0[k1], YH[k1] for k1 <= L/2
+            // lane 0: column spectra Y0[k1], YH[k1] for k1 <= L/2.  The bias
+            // enters at bin (0, 0): with the unnormalised inverse, adding b
+            // there adds b to every pixel of the patch.
+            const float bv = bias ? bias[co] : 0.f;
             auto y0 = [&](int k) {
-                return k == 0 ? make_float2(pa[0].x, 0.f) : (k == H2 ? make_float2(pa[0].y, 0.f) : pa[k]);
+                return k == 0 ? make_float2(pa[0].x + bv, 0.f) : (k == H2 ? make_float2(pa[0].y, 0.f) : pa[k]);
             };
             auto yh = [&](int k) {
                 return k == 0 ? make_float2(pb[0].x, 0.f) : (k == H2 ? make_float2(pb[0].y, 0.f) : pb[k]);
@@ -422,16 +428,25 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
         }
         __syncthreads();
 
-        // store phase: whole band rows, bias and ReLU
+        // store phase: whole band rows, ReLU (the bias is already in the
+        // DC bin, so every pixel of every patch carries it)
         {
-            const float bv = bias ? bias[co] : 0.f;
             const int tl = (t0 + TG < nt ? t0 + TG : nt) - 1;
             const int tr0 = t0 / tw, tr1 = tl / tw;
             // columns of this item's tiles in its first and last tile rows
             const int lo0 = (t0 - tr0 * tw) * T;
             const int hi_last = min((tl - tr1 * tw + 1) * T, w);
+            const int hi_first = tr1 == tr0 ? hi_last : w;
             const int rows_first = min(T, h - (tr0 % th) * T);
             const int rows_last = min(T, h - (tr1 % th) * T);
+            const int last0 = g.slots - rows_last;
+            // whether some float4 of the first or last tile row straddles the
+            // item's column range (the same for every lane of the item)
+            const bool edge = ((lo0 | hi_last) & 3) != 0;
+            const int col = 4 * c4;
+            const bool in_first = col >= lo0 && col + 4 <= hi_first;
+            const bool in_last = col + 4 <= hi_last;
+            const bool lane_ok = lrow < rpi;
             const int sl0 = opaque(slot0);
             const int x0 = sl0 + g.r0;
             int qd = div_small(x0, h, inv_h);
@@ -442,32 +457,31 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
             const float* src = ob + sl0 * obp + 4 * c4;
             // Every lane issues one 16-byte store per slot (dropped through an
             // out-of-range offset where it has nothing to write), so the count
-            // of stores after this item's spectrum loads is fixed; only a
-            // float4 that straddles an item's first or last column takes
-            // four 4-byte stores.
+            // of stores after this item's spectrum loads is fixed; only where
+            // a float4 straddles an item's first or last column (never when
+            // items start and end on tile-row boundaries whose columns are
+            // multiples of 4) are four 4-byte stores added.
 #pragma unroll
             for (int k = 0; k < NV; ++k) {
                 const int sl = sl0 + k * slot_step;
-                const bool ok = lrow < rpi && sl < g.slots;
-                int lo = 0, hi = w;
-                if (sl < rows_first) {
-                    lo = lo0;
-                    if (tr1 == tr0) hi = hi_last;
-                } else if (sl >= g.slots - rows_last) {
-                    hi = hi_last;
-                }
+                const bool ok = lane_ok && sl < g.slots;
+                const bool first = sl < rows_first;
+                const bool last = sl >= last0;
+                const bool full = ok && (first ? in_first : (last ? in_last : true));
                 const float* sp = ok ? src + k * slot_step * obp : ob;
-                float4 v = make_float4(sp[0] + bv, sp[1] + bv, sp[2] + bv, sp[3] + bv);
+                float4 v = make_float4(sp[0], sp[1], sp[2], sp[3]);
                 if (relu) v = make_float4(fmaxf(v.x, 0.f), fmaxf(v.y, 0.f), fmaxf(v.z, 0.f), fmaxf(v.w, 0.f));
-                const int col = 4 * c4;
                 const unsigned soff = unsigned(k * slot_step * w * 4);
-                const bool full = ok && col >= lo && col + 4 <= hi;
                 buf_store_f32x4(v, ryo, full ? voff : kOutOfRange, soff);
-                if (ok && !full && col + 4 > lo && col < hi) {
-                    buf_store_f32(v.x, ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
-                    buf_store_f32(v.y, ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
-                    buf_store_f32(v.z, ryo, col + 2 >= lo && col + 2 < hi ? voff + 8u : kOutOfRange, soff);
-                    buf_store_f32(v.w, ryo, col + 3 >= lo && col + 3 < hi ? voff + 12u : kOutOfRange, soff);
+                if (edge) {
+                    const int lo = first ? lo0 : 0;
+                    const int hi = first ? hi_first : (last ? hi_last : w);
+                    if (ok && !full && col + 4 > lo && col < hi) {
+                        buf_store_f32(v.x, ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
+                        buf_store_f32(v.y, ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
+                        buf_store_f32(v.z, ryo, col + 2 >= lo && col + 2 < hi ? voff + 8u : kOutOfRange, soff);
+                        buf_store_f32(v.w, ryo, col + 3 >= lo && col + 3 < hi ? voff + 12u : kOutOfRange, soff);
+                    }
                 }
                 rr += dr;
                 voff += dq_off;

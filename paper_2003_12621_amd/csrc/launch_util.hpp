@@ -60,6 +60,15 @@ constexpr unsigned kOutOfRange = 0x80000000u;   // offset that is always out of 
 __device__ __forceinline__ BufRsrc make_rsrc(const void* base, unsigned bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
+// A 16-byte load of data read once and not again soon (the filter spectra
+// in the contraction): marked non-temporal, so that streaming it through
+// does not push the patch and output spectra out of the caches.
+__device__ __forceinline__ uint4 load_stream_u4(const uint4* p) {
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    return make_uint4(t.x, t.y, t.z, t.w);
+}
+
 __device__ __forceinline__ float buf_load_f32(BufRsrc r, unsigned voff, unsigned soff) {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
 }

@@ -357,6 +357,7 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_plan_info(fftsplit_plan_t plan, fftsp
     i.contract_stage_k = plan->con_kc;
     i.contract_real_products = plan->con_products;
     i.direct_wspec_bytes = direct_wspec_bytes(*plan);
+    i.spec_group = patch_group(plan->L);
     *out = i;
     return FFTSPLIT_SUCCESS;
 }

@@ -55,6 +55,14 @@ def test_first_config_geometry():
     assert i.yspec_bytes == 8 * i.bins * i.cout_padded * i.tiles_padded
     assert i.yspec_offset >= i.xspec_offset + i.xspec_bytes
     assert i.workspace_bytes >= i.yspec_offset + i.yspec_bytes
+    assert i.spec_group == 64 and i.tiles_padded % i.spec_group == 0
+
+
+@pytest.mark.parametrize("t,group", [(6, 64), (14, 32), (30, 16)])
+def test_output_spectra_group(t, group):
+    """The inverse's unit of work, G patches, by FFT size 8 / 16 / 32."""
+    i = plan(h=64, w=64, tile=t).info
+    assert i.spec_group == group and i.tiles_padded % group == 0
 
 
 @pytest.mark.parametrize("h,w,t,k", [(56, 56, 28, 5), (56, 56, 12, 5), (224, 224, 30, 3), (224, 224, 6, 3),
