@@ -189,7 +189,9 @@ def time_vgg_spatial(args, layers, x, split_stack):
         return a
 
     res = {}
-    for name, fn in (("direct_hip", lambda: direct.forward(xd)), ("torch_conv2d", torch_stack)):
+    oaa = VGG16Stack(layers, batch=VGG_BATCH, tiles=[3] * 13, mode="oaa")
+    for name, fn in (("direct_hip", lambda: direct.forward(xd)), ("torch_conv2d", torch_stack),
+                     ("oaaconv", lambda: oaa.forward(xd))):
         warm_up(fn, None, min_s=0.3)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
@@ -205,6 +207,7 @@ def time_vgg_spatial(args, layers, x, split_stack):
     nt = torch.linalg.vector_norm(yt)
     res["direct_hip"]["rel_l2_vs_torch"] = float(torch.linalg.vector_norm(yd - yt) / nt)
     res["split_rel_l2_vs_torch"] = float(torch.linalg.vector_norm(ys - yt) / nt)
+    res["oaaconv"]["rel_l2_vs_torch"] = float(torch.linalg.vector_norm(oaa.forward(xd) - yt) / nt)
     return res
 
 
@@ -375,9 +378,51 @@ def main():
     }
     if not args.no_compare:
         out["spatial_methods"] = time_spatial_methods(args, plan, layer, xd, wd, bd)
+        out["oaaconv"] = time_oaaconv(args, layer, xd, wd, bd)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layer, x, w, b, tile)
     print(json.dumps(out), flush=True)
+
+
+def time_oaaconv(args, layer, xd, wd, bd):
+    """The same layer by OaAConv, the paper's comparison method (Section 2,
+    Fig. 1): this library's overlap-add pipeline at T = K, L = 2K - 1, timed
+    like the split path (K conv2d steps; stage times from a staged pass)."""
+    import torch
+    import paper_2003_12621_amd as fs
+    k = layer.k
+    plan = fs.Plan(layer.n, layer.cin, layer.h, layer.w, layer.cout, k, tile=k, mode="oaa", bias=bd is not None,
+                   device=0)
+    wspec = plan.transform_weights(wd)
+    ws = plan.new_workspace()
+    y = plan.new_output()
+    warm_up(lambda: plan.conv2d(xd, wspec, bd, out=y, workspace=ws), None, min_s=0.3)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        plan.conv2d(xd, wspec, bd, out=y, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    for e in ev:
+        e.record()
+    torch.cuda.synchronize()
+    fs.set_timing_events(ev[0], ev[1])
+    plan.forward(xd, ws)
+    fs.set_timing_events(ev[2], ev[3])
+    plan.contract(wspec, ws)
+    fs.set_timing_events(ev[4], ev[5])
+    plan.inverse(ws, bias=bd, out=y)
+    fs.set_timing_events()
+    torch.cuda.synchronize()
+    info = plan.info
+    return {"ms": round(ms, 4), "GFLOP/s": round(layer.direct_flops / (ms * 1e-3) / 1e9, 1),
+            "tile": info.tile, "nfft": info.nfft, "tiles": info.tiles, "bins": info.bins,
+            "contract_flops": (8 * info.bins) * layer.cin * layer.cout * info.tiles,
+            "stage_ms": {"forward": round(ev[0].elapsed_time(ev[1]), 4),
+                         "contract": round(ev[2].elapsed_time(ev[3]), 4),
+                         "inverse_and_seams": round(ev[4].elapsed_time(ev[5]), 4)}}
 
 
 def time_spatial_methods(args, plan, layer, xd, wd, bd):

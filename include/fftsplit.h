@@ -53,7 +53,7 @@ typedef struct fftsplit_plan_s* fftsplit_plan_t;   /* opaque, host-side */
 typedef enum {
     FFTSPLIT_SUCCESS = 0,
     FFTSPLIT_ERROR_INVALID_VALUE = 1,        /* bad dimension, NULL/misaligned pointer, aliasing */
-    FFTSPLIT_ERROR_NOT_SUPPORTED = 2,        /* even K, stride != 1, pad != K/2, L not in {8,16,32} */
+    FFTSPLIT_ERROR_NOT_SUPPORTED = 2,        /* even K, stride != 1, pad != K/2, unsupported L */
     FFTSPLIT_ERROR_INSUFFICIENT_WORKSPACE = 3,
     FFTSPLIT_ERROR_DEVICE = 4,               /* a HIP runtime call or kernel launch failed */
     FFTSPLIT_ERROR_ARCH = 5                  /* the device is not gfx950 */
@@ -72,7 +72,11 @@ enum {
  * padding of k/2 (Section 2, eq. 1; Section 3.1). */
 typedef struct {
     int n, cin, h, w, cout, k;
-    int tile;        /* T; 0 lets the plan choose among L = 8, 16, 32 */
+    int tile;        /* T; 0 lets the plan choose among L = 8, 16, 32.  With
+                      * FFTSPLIT_OVERLAP_ADD, tile = k (k = 3, 5, 7) selects the
+                      * OaAConv configuration the paper compares against
+                      * (Section 2, Fig. 1): patches of the filter's size,
+                      * L = 2k - 1 = 5, 9, 13 */
     int stride;      /* must be 1 */
     int pad;         /* must be k/2 ('same') */
     unsigned flags;  /* FFTSPLIT_* flags above */
@@ -92,6 +96,10 @@ typedef struct {
  *   f = L*L/2 - 1                 (S(0, L/2), S(L/2, L/2)) as (re, im)
  * The two last slots are multiplied part by part in the per-bin product
  * (a product of two real bins is real), the others as complex numbers.
+ * For odd L (the OaAConv configuration) only S(0, 0) is real, nothing is
+ * packed, and bins = (L*L+1)/2:
+ *   f = (k2-1)*L + k1             S(k1, k2)   for k2 in [1, (L-1)/2], k1 in [0, L)
+ *   f = (L-1)/2*L + k1            S(k1, 0)    for k1 in [0, (L-1)/2]
  *
  * Patch index t = (img * tiles_h + a) * tiles_w + b for the patch whose
  * top-left output pixel is (a*T, b*T); t in [tiles, tiles_padded) are zero
@@ -116,7 +124,7 @@ typedef struct {
     int tiles_h, tiles_w;/* ceil(h/T), ceil(w/T) */
     int tiles;           /* n * tiles_h * tiles_w */
     int tiles_padded;    /* tiles rounded up to the contraction's tile granularity */
-    int bins;            /* L*L/2 */
+    int bins;            /* L*L/2 ((L*L+1)/2 for odd L) */
     int cout_padded;     /* cout rounded up to the contraction's tile granularity */
     unsigned flags;
     size_t wspec_bytes;

@@ -324,8 +324,11 @@ def bin_coords(L: int):
     """Stored bins of an L x L real transform, in the library's order
     (fftsplit.h): a list of L*L/2 entries.  Entry f is (k1, k2) for a complex
     bin; the last two entries are pairs ((k1, k2) of the real part,
-    (k1, k2) of the imaginary part) for the slots holding two real bins."""
+    (k1, k2) of the imaginary part) for the slots holding two real bins.
+    Odd L (the OaAConv configuration): (L*L+1)/2 complex bins, none packed."""
     h2 = L // 2
+    if L % 2:
+        return [(k1, k2) for k2 in range(1, h2 + 1) for k1 in range(L)] + [(k1, 0) for k1 in range(h2 + 1)]
     coords = []
     for k2 in range(1, h2):
         for k1 in range(L):

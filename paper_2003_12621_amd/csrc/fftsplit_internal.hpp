@@ -43,8 +43,11 @@ constexpr int kTileGranule = 64;
 constexpr int kCoutGranule = 64;
 
 // Patches per work item of the forward/inverse transforms (L/2 threads
-// each), by FFT size.
-__host__ __device__ constexpr int patch_group(int L) { return L == 8 ? 64 : (L == 16 ? 32 : 16); }
+// each), by FFT size; the odd sizes of the OaAConv configuration transform
+// one patch per thread and group patches in 64s.
+__host__ __device__ constexpr int patch_group(int L) {
+    return L % 2 ? 64 : (L == 8 ? 64 : (L == 16 ? 32 : 16));
+}
 
 // Patch stride (float2) of the half spectra in the band variant of the
 // forward transform: L rows of L/2+1 bins, plus one to make it odd.
@@ -80,7 +83,15 @@ __host__ __device__ inline size_t yspec_offset(int c, int f, int t, int bins, in
 // complex bins k1 in [1, L/2-1] are stored, and their four real bins
 // (k1, k2 in {0, L/2}) share two slots: real_a = (S(0,0), S(L/2,0)),
 // real_b = (S(0,L/2), S(L/2,L/2)) as (re, im).
-__host__ __device__ constexpr int stored_bins(int L) { return L * L / 2; }
+//
+// Odd L (the OaAConv configuration, L = 2K - 1): no column is real, only
+// the bin (0, 0); (L*L+1)/2 slots, none packed:
+//   f = (k2-1)*L + k1      S(k1, k2)  for k2 in [1, (L-1)/2], k1 in [0, L)
+//   f = (L-1)/2*L + k1     S(k1, 0)   for k1 in [0, (L-1)/2]
+__host__ __device__ constexpr int stored_bins(int L) { return L % 2 ? (L * L + 1) / 2 : L * L / 2; }
+// slots at the end that each hold two real bins (multiplied part by part)
+__host__ __device__ constexpr int packed_slots(int L) { return L % 2 ? 0 : 2; }
+__host__ __device__ constexpr int bin_odd_col0(int L, int k1) { return (L / 2) * L + k1; }
 __host__ __device__ constexpr int bin_mid(int L, int k1, int k2) { return (k2 - 1) * L + k1; }
 // complex bins of the real columns, k1 in [1, L/2-1]
 __host__ __device__ constexpr int bin_col0(int L, int k1) { return L * (L / 2 - 1) + k1 - 1; }
@@ -105,6 +116,14 @@ hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xspec, const 
 hipError_t launch_inverse(const fftsplit_plan_s& p, const float2* yspec, const float* bias, float* y, void* aux,
                           hipStream_t s, const LaunchEvents& ev);
 hipError_t launch_maxpool(const float* x, float* y, int n, int c, int h, int w, hipStream_t s);
+// OaAConv configuration (odd L = 2K - 1, T = K, overlap-add): k_oaa.hip
+hipError_t launch_oaa_forward(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s,
+                              const LaunchEvents& ev);
+hipError_t launch_oaa_inverse(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y, float* aux,
+                              hipStream_t s, const LaunchEvents& ev);
+// overlap-add seams from the per-patch L x L results in aux (k_inverse.hip)
+hipError_t launch_seam(const fftsplit_plan_s& p, const float* aux, const float* bias, float* y, hipStream_t s,
+                       hipEvent_t stop);
 size_t direct_wspec_bytes(const fftsplit_plan_s& p);
 hipError_t launch_direct_weights(const fftsplit_plan_s& p, const float* w, float* wd, hipStream_t s);
 hipError_t launch_direct(const fftsplit_plan_s& p, const float* x, const float* wd, const float* bias, float* y,

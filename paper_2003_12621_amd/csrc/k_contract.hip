@@ -58,7 +58,7 @@ struct ConShape {
 template <int BM, int BN, int KC, int WM, bool G3>
 __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict__ xs, const float2* __restrict__ ws,
                                                        float2* __restrict__ ys, int cin, int coutp, int ntp,
-                                                       int nbco, int nbt, int nbins, int ygroup) {
+                                                       int nbco, int nbt, int nbins, int ygroup, int npacked) {
     using S = ConShape<BM, BN, KC, WM>;
     constexpr int TM = S::TM, TN = S::TN;
     extern __shared__ float4 lds_raw[];
@@ -74,9 +74,9 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     const int rest = lb / nbco;
     const int tbk = rest % nbt;
     const int f = rest / nbt;
-    // the last two bins are slots of two real bins each (fftsplit.h): their
-    // products are taken component by component
-    const bool packed = f >= nbins - 2;
+    // the last two bins (even L) are slots of two real bins each
+    // (fftsplit.h): their products are taken component by component
+    const bool packed = f >= nbins - npacked;
     const int co0 = cbk * BM;
     const int t0 = tbk * BN;
 
@@ -254,7 +254,7 @@ static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, 
     const int nbco = p.coutp / BM, nbt = p.ntp / BN;
     const size_t nb = size_t(nbco) * nbt * p.bins;
     return launch_kernel(kern, dim3(unsigned(nb)), dim3(S::NT), S::LDS_BYTES, s, ev.start, ev.stop, xs, ws, ys,
-                         p.prob.cin, p.coutp, p.ntp, nbco, nbt, p.bins, patch_group(p.L));
+                         p.prob.cin, p.coutp, p.ntp, nbco, nbt, p.bins, patch_group(p.L), packed_slots(p.L));
 }
 
 hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xs, const float2* ws, float2* ys,

@@ -479,6 +479,7 @@ static hipError_t launch_forward_band(const fftsplit_plan_s& p, const float* x, 
 
 hipError_t launch_forward(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s,
                           const LaunchEvents& ev) {
+    if (p.L % 2) return launch_oaa_forward(p, x, xs, s, ev);
     if (p.fwd_band) {
         switch (p.L) {
             case 8: return launch_forward_band<8, 64, kBandNV8>(p, x, xs, s, ev);

@@ -540,8 +540,13 @@ static hipError_t launch_inverse_v(const fftsplit_plan_s& p, const float2* ys, c
                                  bias, y, aux, p.prob.cout, p.coutp, p.prob.h, p.prob.w, p.T, p.P, p.th, p.tw, p.nt,
                                  p.ntp, ngroups, int(p.relu), p.prob.n * p.prob.cout * p.prob.h * p.prob.w);
     if (e != hipSuccess || !OAA) return e;
+    return launch_seam(p, aux, bias, y, s, ev.stop);
+}
+
+hipError_t launch_seam(const fftsplit_plan_s& p, const float* aux, const float* bias, float* y, hipStream_t s,
+                       hipEvent_t stop) {
     const dim3 sgrid(unsigned((p.prob.h * p.prob.w + 255) / 256), unsigned(p.prob.n * p.prob.cout));
-    return launch_kernel(seam_kernel, sgrid, dim3(256), 0, s, nullptr, ev.stop, aux, bias, y, p.prob.cout, p.prob.h,
+    return launch_kernel(seam_kernel, sgrid, dim3(256), 0, s, nullptr, stop, aux, bias, y, p.prob.cout, p.prob.h,
                          p.prob.w, p.T, p.P, p.L, p.th, p.tw, p.ntp, int(p.relu));
 }
 
@@ -556,6 +561,7 @@ hipError_t launch_inverse(const fftsplit_plan_s& p, const float2* ys, const floa
                           hipStream_t s, const LaunchEvents& ev) {
     float* a = static_cast<float*>(aux);
     if (p.oaa && !a) return hipErrorInvalidValue;
+    if (p.L % 2) return launch_oaa_inverse(p, ys, bias, y, a, s, ev);
     if (p.inv_band) {
         switch (p.L) {
             case 8: return launch_inverse_band<8, 64, kBandNV8>(p, ys, bias, y, s, ev);

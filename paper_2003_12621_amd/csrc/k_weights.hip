@@ -37,7 +37,15 @@ __global__ __launch_bounds__(256) void weights_kernel(const float* __restrict__ 
     // real part and (k1b, k2b) in its imaginary part.
     const int h2 = L / 2;
     int k1, k2, k1b = -1, k2b = -1;
-    if (f < L * (h2 - 1)) {
+    if (L % 2) {   // odd L: complex columns k2 in [1, (L-1)/2], then half of column 0
+        if (f < h2 * L) {
+            k2 = 1 + f / L;
+            k1 = f % L;
+        } else {
+            k2 = 0;
+            k1 = f - h2 * L;
+        }
+    } else if (f < L * (h2 - 1)) {
         k2 = 1 + f / L;
         k1 = f % L;
     } else if (f < L * (h2 - 1) + h2 - 1) {
@@ -51,7 +59,7 @@ __global__ __launch_bounds__(256) void weights_kernel(const float* __restrict__ 
         k1b = h2;
         k2 = k2b = f == L * h2 - 2 ? 0 : h2;
     }
-    const int step = kTwN / L;
+    const int step = L % 2 ? 1 : kTwN / L;   // odd L: the table holds its own L entries
     const float* wp = w + (size_t(co) * cin + ci) * K * K;
     // conj(sum w exp(-2 pi i e / L)) = sum w exp(+2 pi i e / L), e = u k1 + v k2
     auto spectrum = [&](int a, int b, double& re, double& im) {
@@ -79,10 +87,18 @@ __global__ __launch_bounds__(256) void weights_kernel(const float* __restrict__ 
 
 hipError_t launch_weights(const fftsplit_plan_s& p, const float* w, float2* wspec, hipStream_t s,
                           const LaunchEvents& ev) {
-    TwiddlesD tw;
-    for (int i = 0; i < kTwN; ++i) {
-        tw.c[i] = kTwCosD[i];
-        tw.s[i] = kTwSinD[i];
+    TwiddlesD tw{};
+    const double* tc = kTwCosD;
+    const double* ts = kTwSinD;
+    int nt = kTwN;
+    switch (p.L) {
+        case 5: tc = kTw5CosD; ts = kTw5SinD; nt = 5; break;
+        case 9: tc = kTw9CosD; ts = kTw9SinD; nt = 9; break;
+        case 13: tc = kTw13CosD; ts = kTw13SinD; nt = 13; break;
+    }
+    for (int i = 0; i < nt; ++i) {
+        tw.c[i] = tc[i];
+        tw.s[i] = ts[i];
     }
     const size_t total = size_t(p.bins) * p.prob.cin * p.coutp;
     const unsigned blocks = unsigned((total + 255) / 256);

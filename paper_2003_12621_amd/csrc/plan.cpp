@@ -73,6 +73,11 @@ static Geometry geometry(const fftsplit_problem_t& p, int L) {
 
 static bool supported_L(int L) { return L == 8 || L == 16 || L == 32; }
 
+// The OaAConv configuration (the paper's comparison method, Section 2 and
+// Fig. 1): overlap-add with patches of the filter's size, T = K, so the
+// transforms are L = 2K - 1 = 5, 9 or 13 points.
+static bool oaaconv_L(int L, int k, bool oaa) { return oaa && L == 2 * k - 1 && (k == 3 || k == 5 || k == 7); }
+
 // The band variant of the inverse transform (overlap-save, width a multiple
 // of 4 and at most 256): used when the output band of any work item fits the
 // store slots it assigns and its LDS stays within two workgroups per compute
@@ -179,9 +184,10 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     Geometry g{};
     if (tile > 0) {
         const int L = tile + p.k - 1;
-        if (!supported_L(L))
+        if (!supported_L(L) && !oaaconv_L(L, p.k, oaa))
             return fail(FFTSPLIT_ERROR_NOT_SUPPORTED,
-                        "tile + k - 1 must be 8, 16 or 32 (got " + std::to_string(L) + ")");
+                        "tile + k - 1 must be 8, 16 or 32, or tile = k for k in {3, 5, 7} with overlap-add "
+                        "(got " + std::to_string(L) + ")");
         g = geometry(p, L);
     } else {
         bool have = false;

@@ -11,9 +11,13 @@ import numpy as np
 
 
 def stored_coords(L: int):
-    """(k1, k2) of every complex stored bin, in the header's order; the two
-    slots that follow them hold the real bins of real_pairs(L)."""
+    """(k1, k2) of every complex stored bin, in the header's order; for even
+    L the two slots that follow them hold the real bins of real_pairs(L).
+    Odd L (the OaAConv sizes): columns k2 in [1, (L-1)/2], then k1 in
+    [0, (L-1)/2] of column 0, nothing packed."""
     h2 = L // 2
+    if L % 2:
+        return [(k1, k2) for k2 in range(1, h2 + 1) for k1 in range(L)] + [(k1, 0) for k1 in range(h2 + 1)]
     out = [(k1, k2) for k2 in range(1, h2) for k1 in range(L)]
     out += [(k1, 0) for k1 in range(1, h2)]
     out += [(k1, h2) for k1 in range(1, h2)]
@@ -23,6 +27,8 @@ def stored_coords(L: int):
 def real_pairs(L: int):
     """The last two stored slots: (bin in the real part, bin in the imaginary part)."""
     h2 = L // 2
+    if L % 2:
+        return []
     return [((0, 0), (h2, 0)), ((0, h2), (h2, h2))]
 
 
@@ -32,7 +38,7 @@ def full_to_stored(full: np.ndarray) -> np.ndarray:
     k1, k2 = np.array(stored_coords(L)).T
     st = np.moveaxis(full[..., k1, k2], -1, 0).astype(np.complex128)
     packed = [full[..., a[0], a[1]].real + 1j * full[..., b[0], b[1]].real for a, b in real_pairs(L)]
-    return np.concatenate([st, np.stack(packed)], axis=0)
+    return np.concatenate([st, np.stack(packed)], axis=0) if packed else st
 
 
 def stored_to_full(stored: np.ndarray, L: int) -> np.ndarray:

@@ -165,15 +165,43 @@ def test_bin_order_matches_header():
                 assert (k1, k2) in stored or mirror in stored
 
 
+@pytest.mark.parametrize("L", [5, 9, 13])
+def test_odd_bin_order(L):
+    """The OaAConv sizes: (L*L+1)/2 complex bins, every bin of the real
+    transform stored once or as the conjugate of a stored one."""
+    from spectra_layout import stored_coords
+    coords = fs.bin_coords(L)
+    assert coords == stored_coords(L)
+    assert len(coords) == (L * L + 1) // 2 == len(set(coords))
+    for k1 in range(L):
+        for k2 in range(L):
+            mirror = ((-k1) % L, (-k2) % L)
+            assert ((k1, k2) in coords) != (mirror in coords) or (k1, k2) == mirror == (0, 0)
+
+
+@pytest.mark.parametrize("k", [3, 5, 7])
+def test_oaaconv_plan(k):
+    """Overlap-add with tile = k gives the OaAConv transform size 2k - 1."""
+    p = plan(n=2, cin=8, h=30, w=31, cout=8, k=k, tile=k, mode="oaa")
+    i = p.info
+    L = 2 * k - 1
+    assert (i.tile, i.nfft, i.bins) == (k, L, (L * L + 1) // 2)
+    assert (i.tiles_h, i.tiles_w) == (-(-30 // k), -(-31 // k))
+    assert i.aux_bytes == 4 * 8 * i.tiles_padded * L * L
+    # odd sizes exist only for that configuration
+    assert status_of(n=2, cin=8, h=30, w=31, cout=8, k=k, tile=k) == fs.ERROR_NOT_SUPPORTED
+    assert status_of(n=2, cin=8, h=30, w=31, cout=8, k=k, tile=k + 2, mode="oaa") == fs.ERROR_NOT_SUPPORTED
+
+
 def test_spectra_layout_helpers_roundtrip():
     import numpy as np
     from spectra_layout import full_to_stored, stored_to_full, rel_l2
     rng = np.random.default_rng(3)
-    for L in (8, 16, 32):
+    for L in (8, 16, 32, 5, 9, 13):
         a = rng.standard_normal((2, 3, L, L))
         full = np.fft.fft2(a)
         st = full_to_stored(full)
-        assert st.shape == (L * L // 2, 2, 3)
+        assert st.shape == ((L * L + 1) // 2, 2, 3)
         np.testing.assert_allclose(stored_to_full(st, L), full, rtol=0, atol=1e-12)
     # the error measure sees imaginary parts
     assert rel_l2(np.array([1 + 1j]), np.array([1 + 0j])) == 1.0

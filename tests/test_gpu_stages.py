@@ -30,7 +30,15 @@ CASES = [
     ("ragged_L32", (3, 4, 37, 30, 7, 3), 30),
     ("k1_L8", (1, 2, 17, 9, 3, 1), 8),
     ("k7_L16", (1, 3, 21, 20, 5, 7), 10),
+    # the OaAConv configuration (overlap-add, T = K, odd L = 2K - 1)
+    ("oaa_k3_L5", (2, 5, 19, 23, 10, 3), 3),
+    ("oaa_k5_L9", (1, 3, 21, 20, 70, 5), 5),
+    ("oaa_k7_L13", (2, 17, 17, 30, 7, 7), 7),
 ]
+
+
+def _oaaconv(shape, tile):
+    return tile == shape[5] and tile in (3, 5, 7)
 
 
 def _dev(a):
@@ -39,6 +47,8 @@ def _dev(a):
 
 def _setup(shape, tile, mode="os", seed=5):
     n, cin, h, w, cout, k = shape
+    if _oaaconv(shape, tile):
+        mode = "oaa"
     x, wt = small_layer(n, cin, h, w, cout, k, seed=seed)
     plan = fs.Plan(n, cin, h, w, cout, k, tile=tile, mode=mode)
     return x, wt, plan
@@ -64,6 +74,8 @@ def test_forward_spectra(name, shape, tile, mode):
     n, cin, h, w, cout, k = shape
     if mode == "oaa" and tile < k - 1:
         pytest.skip("overlap-add needs T >= K - 1")
+    if mode == "os" and _oaaconv(shape, tile):
+        pytest.skip("the OaAConv configuration is overlap-add only")
     x, wt, plan = _setup(shape, tile, mode)
     ws = plan.new_workspace()
     plan.forward(_dev(x), ws)
@@ -94,9 +106,9 @@ def test_contraction(name, shape, tile):
     # filter spectra are already conjugated, so they enter as conj(W).
     ref = oracle.hadamard_channel_sum(X.transpose(2, 1, 0), np.conj(W).transpose(2, 1, 0))  # [t, co, bins]
     ref = ref.transpose(2, 1, 0)                                    # [bins, co, t]
-    # the last two slots each hold two real bins (real and imaginary part):
-    # their products are taken part by part
-    for f in (-2, -1):
+    # for even L the last two slots each hold two real bins (real and
+    # imaginary part): their products are taken part by part
+    for f in ((-2, -1) if plan.nfft % 2 == 0 else ()):
         ref[f] = (np.einsum("ic,it->ct", W[f].real, X[f].real)
                   + 1j * np.einsum("ic,it->ct", W[f].imag, X[f].imag))
     assert rel_l2(Y, ref) < 2e-6
@@ -108,6 +120,8 @@ def test_contraction(name, shape, tile):
 @pytest.mark.parametrize("name,shape,tile", CASES)
 def test_inverse_placement(name, shape, tile, relu, mode):
     n, cin, h, w, cout, k = shape
+    if mode == "os" and _oaaconv(shape, tile):
+        pytest.skip("the OaAConv configuration is overlap-add only")
     x, wt = small_layer(n, cin, h, w, cout, k, seed=6)
     plan = fs.Plan(n, cin, h, w, cout, k, tile=tile, bias=True, relu=relu, mode=mode)
     L = plan.nfft
