@@ -64,7 +64,10 @@ enum {
     FFTSPLIT_OVERLAP_SAVE = 0,   /* halo'd patches, crop + concatenate (Section 3.1); default */
     FFTSPLIT_OVERLAP_ADD  = 1,   /* zero-padded patches, overlap-add of the L x L results */
     FFTSPLIT_BIAS         = 2,   /* add bias[co] in the inverse stage */
-    FFTSPLIT_RELU         = 4    /* apply max(., 0) after the bias */
+    FFTSPLIT_RELU         = 4,   /* apply max(., 0) after the bias */
+    FFTSPLIT_MAXPOOL      = 8    /* then a 2x2 stride-2 max-pool (floor): y is
+                                  * [n][cout][h/2][w/2] (the VGG stage ends);
+                                  * needs h, w >= 2 */
 };
 
 /* The layer, as the paper states the problem: batch n, channels cin -> cout,

@@ -34,6 +34,7 @@ OVERLAP_SAVE = 0
 OVERLAP_ADD = 1
 BIAS = 2
 RELU = 4
+MAXPOOL = 8
 
 
 class Problem(ctypes.Structure):
@@ -143,19 +144,30 @@ def _dev_tensor(t, name: str, dtype=None, numel: Optional[int] = None):
     return ctypes.c_void_p(t.data_ptr())
 
 
-def problem(n, cin, h, w, cout, k, tile=0, mode="os", bias=False, relu=False, stride=1, pad=None) -> Problem:
-    flags = (OVERLAP_ADD if mode == "oaa" else OVERLAP_SAVE) | (BIAS if bias else 0) | (RELU if relu else 0)
+def problem(n, cin, h, w, cout, k, tile=0, mode="os", bias=False, relu=False, stride=1, pad=None,
+            pool=False) -> Problem:
+    flags = ((OVERLAP_ADD if mode == "oaa" else OVERLAP_SAVE) | (BIAS if bias else 0) | (RELU if relu else 0)
+             | (MAXPOOL if pool else 0))
     if mode not in ("os", "oaa"):
         raise ValueError("mode must be 'os' or 'oaa'")
     return Problem(n, cin, h, w, cout, k, tile, stride, k // 2 if pad is None else pad, flags)
+
+
+def _prod(shape):
+    p = 1
+    for v in shape:
+        p *= v
+    return p
 
 
 class Plan:
     """A validated layer plan (host-side).  See fftsplit.h for every field."""
 
     def __init__(self, n, cin, h, w, cout, k, tile=0, mode="os", bias=False, relu=False, device=None,
-                 arch: Optional[str] = None, stride=1, pad=None):
-        self.prob = problem(n, cin, h, w, cout, k, tile, mode, bias, relu, stride, pad)
+                 arch: Optional[str] = None, stride=1, pad=None, pool=False):
+        """pool=True appends the 2x2 stride-2 max-pool (FFTSPLIT_MAXPOOL):
+        outputs are [n, cout, h // 2, w // 2]."""
+        self.prob = problem(n, cin, h, w, cout, k, tile, mode, bias, relu, stride, pad, pool)
         handle = ctypes.c_void_p()
         if arch is not None:
             _check(lib().fftsplit_plan_for_arch(ctypes.byref(self.prob), arch.encode(), ctypes.byref(handle)),
@@ -171,7 +183,7 @@ class Plan:
         _check(lib().fftsplit_plan_info(self._h, ctypes.byref(info)), "fftsplit_plan_info")
         self.info = info
         self.n, self.cin, self.h, self.w, self.cout, self.k = n, cin, h, w, cout, k
-        self.mode, self.has_bias, self.relu = mode, bias, relu
+        self.mode, self.has_bias, self.relu, self.pool = mode, bias, relu, pool
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -192,9 +204,15 @@ class Plan:
         torch = _torch()
         return torch.empty(self.info.workspace_bytes, dtype=torch.uint8, device=self.device)
 
+    @property
+    def out_shape(self):
+        if self.pool:
+            return (self.n, self.cout, self.h // 2, self.w // 2)
+        return (self.n, self.cout, self.h, self.w)
+
     def new_output(self):
         torch = _torch()
-        return torch.empty((self.n, self.cout, self.h, self.w), dtype=torch.float32, device=self.device)
+        return torch.empty(self.out_shape, dtype=torch.float32, device=self.device)
 
     # -- entry points ---------------------------------------------------
     def transform_weights(self, w, out=None):
@@ -213,7 +231,7 @@ class Plan:
         torch = _torch()
         xp = _dev_tensor(x, "x", torch.float32, self.n * self.cin * self.h * self.w)
         out = self.new_output() if out is None else out
-        yp = _dev_tensor(out, "y", torch.float32, self.n * self.cout * self.h * self.w)
+        yp = _dev_tensor(out, "y", torch.float32, _prod(self.out_shape))
         ws = self.new_workspace() if workspace is None else workspace
         bp = None if bias is None else _dev_tensor(bias, "bias", torch.float32, self.cout)
         _check(lib().fftsplit_conv2d(self._h, xp, _dev_tensor(wspec, "wspec"), bp, yp, _dev_tensor(ws, "workspace"),
@@ -236,7 +254,7 @@ class Plan:
     def inverse(self, workspace, bias=None, out=None):
         torch = _torch()
         out = self.new_output() if out is None else out
-        yp = _dev_tensor(out, "y", torch.float32, self.n * self.cout * self.h * self.w)
+        yp = _dev_tensor(out, "y", torch.float32, _prod(self.out_shape))
         bp = None if bias is None else _dev_tensor(bias, "bias", torch.float32, self.cout)
         _check(lib().fftsplit_inverse(self._h, bp, yp, _dev_tensor(workspace, "workspace"),
                                       workspace.numel() * workspace.element_size(), _stream_handle(self.device)),

@@ -71,9 +71,28 @@ fftsplit_status_t launched(hipError_t e, const char* what) {
 }
 
 size_t x_bytes(fftsplit_plan_t p) { return size_t(p->prob.n) * p->prob.cin * p->prob.h * p->prob.w * 4; }
-size_t y_bytes(fftsplit_plan_t p) { return size_t(p->prob.n) * p->prob.cout * p->prob.h * p->prob.w * 4; }
-
 char* ws_at(void* ws, size_t off) { return static_cast<char*>(ws) + off; }
+
+size_t y_bytes(fftsplit_plan_t p) {
+    const size_t plane = p->pool ? size_t(p->prob.h / 2) * (p->prob.w / 2) : size_t(p->prob.h) * p->prob.w;
+    return size_t(p->prob.n) * p->prob.cout * plane * 4;
+}
+
+// The inverse stage into y: with FFTSPLIT_MAXPOOL either pooled in the
+// inverse kernel itself or through the workspace's unpooled staging buffer
+// and a pooling pass.
+hipError_t launch_inverse_to_y(fftsplit_plan_t plan, const float2* ys, const float* bias, float* y, void* workspace,
+                               hipStream_t stream, const LaunchEvents& ev) {
+    void* aux = plan->aux_bytes ? ws_at(workspace, plan->aux_off) : nullptr;
+    if (!plan->pool || plan->pool_fused) return launch_inverse(*plan, ys, bias, y, aux, stream, ev);
+    float* pre = reinterpret_cast<float*>(ws_at(workspace, plan->pre_off));
+    LaunchEvents first;
+    first.start = ev.start;
+    const hipError_t e = launch_inverse(*plan, ys, bias, pre, aux, stream, first);
+    if (e != hipSuccess) return e;
+    return launch_maxpool(pre, y, plan->prob.n, plan->prob.cout, plan->prob.h, plan->prob.w, stream, ev.stop);
+}
+
 
 }  // namespace
 
@@ -132,8 +151,8 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_inverse(fftsplit_plan_t plan, const f
         return fail(FFTSPLIT_ERROR_INVALID_VALUE, "y overlaps the workspace");
     DeviceGuard g(plan->device);
     if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
-    return launched(launch_inverse(*plan, reinterpret_cast<const float2*>(ws_at(workspace, plan->yspec_off)), bias, y,
-                                   plan->aux_bytes ? ws_at(workspace, plan->aux_off) : nullptr, stream, t_events),
+    return launched(launch_inverse_to_y(plan, reinterpret_cast<const float2*>(ws_at(workspace, plan->yspec_off)),
+                                        bias, y, workspace, stream, t_events),
                     "inverse patch transform launch");
 }
 
@@ -164,9 +183,7 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_conv2d(fftsplit_plan_t plan, const fl
     if (fftsplit_status_t s = launched(launch_contract(*plan, xs, static_cast<const float2*>(wspec), ys, stream, middle),
                                        "contraction launch"))
         return s;
-    return launched(launch_inverse(*plan, ys, bias, y, plan->aux_bytes ? ws_at(workspace, plan->aux_off) : nullptr,
-                                   stream, last),
-                    "inverse patch transform launch");
+    return launched(launch_inverse_to_y(plan, ys, bias, y, workspace, stream, last), "inverse patch transform launch");
 }
 
 FFTSPLIT_EXPORT fftsplit_status_t fftsplit_maxpool2x2(const float* x, float* y, int n, int c, int h, int w,
@@ -206,6 +223,7 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_direct_conv2d(fftsplit_plan_t plan, c
         return fail(FFTSPLIT_ERROR_INVALID_VALUE, "y overlaps wd");
     if (x_bytes(plan) > 0x7fffffffu)
         return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "direct convolution: the input must be under 2 GiB");
+    if (plan->pool) return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "direct convolution: FFTSPLIT_MAXPOOL is not supported");
     DeviceGuard g(plan->device);
     if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
     return launched(launch_direct(*plan, x, wd, bias, y, stream, t_events), "direct convolution launch");

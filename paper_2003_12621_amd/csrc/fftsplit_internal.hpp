@@ -18,7 +18,7 @@ struct fftsplit_plan_s {
     int T, L, P;                // tile, FFT size, K/2
     int th, tw, nt, ntp;        // tile grid, tiles, padded tiles
     int bins, coutp;            // stored bins, padded output channels
-    bool oaa, bias, relu;
+    bool oaa, bias, relu, pool;
     size_t wspec_bytes;
     size_t xspec_off, xspec_bytes, yspec_off, yspec_bytes, aux_off, aux_bytes;
     size_t ws_bytes;
@@ -34,6 +34,11 @@ struct fftsplit_plan_s {
     // inv_band; LDS pitch of the output band and dynamic LDS bytes
     bool inv_band;
     int inv_obp, inv_lds;
+    // FFTSPLIT_MAXPOOL: pooled inside the band inverse's store phase if
+    // pool_fused, else the inverse writes the unpooled output to the
+    // workspace at pre_off and a pooling pass follows
+    bool pool_fused;
+    size_t pre_off, pre_bytes;
 };
 
 namespace fftsplit {
@@ -115,7 +120,8 @@ hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xspec, const 
                            hipStream_t s, const LaunchEvents& ev);
 hipError_t launch_inverse(const fftsplit_plan_s& p, const float2* yspec, const float* bias, float* y, void* aux,
                           hipStream_t s, const LaunchEvents& ev);
-hipError_t launch_maxpool(const float* x, float* y, int n, int c, int h, int w, hipStream_t s);
+hipError_t launch_maxpool(const float* x, float* y, int n, int c, int h, int w, hipStream_t s,
+                          hipEvent_t stop = nullptr);
 // OaAConv configuration (odd L = 2K - 1, T = K, overlap-add): k_oaa.hip
 hipError_t launch_oaa_forward(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s,
                               const LaunchEvents& ev);

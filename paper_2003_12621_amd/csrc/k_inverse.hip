@@ -271,7 +271,7 @@ __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux
 //     in the first and last tile row of an item only the columns of its own
 //     tiles are written;
 //   * LDS strides are odd, so the lanes of a wave spread over the banks.
-template <int L, int TG, int NV>
+template <int L, int TG, int NV, bool POOL>
 __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     const float2* __restrict__ ys, const float* __restrict__ bias, float* __restrict__ y, int cout, int coutp, int h,
     int w, int T, int th, int tw, int nt, int ntp, int ngroups, int nitems, int ipw, int obp, int relu,
@@ -428,6 +428,65 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
         }
         __syncthreads();
 
+        // store phase with the 2x2 max-pool (POOL): the band's slots pair up
+        // into pooled rows (tile rows start on even image rows and hold an
+        // even number of rows, and the image height is even), each lane
+        // reads 4 columns of 2 slots and writes 2 pooled values (8 bytes)
+        if constexpr (POOL) {
+            const int hp = h >> 1, wp = w >> 1;
+            const int tl = (t0 + TG < nt ? t0 + TG : nt) - 1;
+            const int tr0 = t0 / tw, tr1 = tl / tw;
+            // pooled columns of this item's tiles in its first and last tile rows
+            const int lo0 = ((t0 - tr0 * tw) * T) >> 1;
+            const int hi_last = min((tl - tr1 * tw + 1) * T, w) >> 1;
+            const int hi_first = tr1 == tr0 ? hi_last : wp;
+            const int rows_first = min(T, h - (tr0 % th) * T) >> 1;
+            const int rows_last = min(T, h - (tr1 % th) * T) >> 1;
+            const int pslots = g.slots >> 1;
+            const int last0 = pslots - rows_last;
+            const bool edge = ((lo0 | hi_last) & 1) != 0;
+            const int col = 2 * c4;
+            const bool in_first = col >= lo0 && col + 2 <= hi_first;
+            const bool in_last = col + 2 <= hi_last;
+            const bool lane_ok = lrow < rpi;
+            const unsigned crossp = unsigned(cout - 1) * unsigned(hp) * unsigned(wp) * 4u;
+            const int dqp = slot_step / hp, drp = slot_step - dqp * hp;
+            const int sl0 = opaque(slot0);
+            const int x0 = sl0 + (g.r0 >> 1);
+            int qd = div_small(x0, hp, 2.f * inv_h);
+            int rr = x0 - qd * hp;
+            unsigned voff = unsigned((((g.img0 * cout + co) * hp + (g.r0 >> 1)) * wp) * 4) + unsigned(sl0 * wp * 4) +
+                            unsigned(8 * c4) + unsigned(qd) * crossp;
+            const unsigned dq_off = unsigned(dqp) * crossp;
+            const float* src = ob + 2 * sl0 * obp + 4 * c4;
+#pragma unroll
+            for (int k = 0; k < (NV + 1) / 2; ++k) {
+                const int ps = sl0 + k * slot_step;
+                const bool ok = lane_ok && ps < pslots;
+                const bool first = ps < rows_first;
+                const bool last = ps >= last0;
+                const bool full = ok && (first ? in_first : (last ? in_last : true));
+                const float* sp = ok ? src + 2 * k * slot_step * obp : ob;
+                float2 v = make_float2(fmaxf(fmaxf(sp[0], sp[1]), fmaxf(sp[obp], sp[obp + 1])),
+                                       fmaxf(fmaxf(sp[2], sp[3]), fmaxf(sp[obp + 2], sp[obp + 3])));
+                if (relu) v = make_float2(fmaxf(v.x, 0.f), fmaxf(v.y, 0.f));
+                const unsigned soff = unsigned(k * slot_step * wp * 4);
+                buf_store_f32x2(v, ryo, full ? voff : kOutOfRange, soff);
+                if (edge) {
+                    const int lo = first ? lo0 : 0;
+                    const int hi = first ? hi_first : (last ? hi_last : wp);
+                    if (ok && !full && col + 2 > lo && col < hi) {
+                        buf_store_f32(v.x, ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
+                        buf_store_f32(v.y, ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
+                    }
+                }
+                rr += drp;
+                voff += dq_off;
+                const bool carry = rr >= hp;
+                rr -= carry ? hp : 0;
+                voff += carry ? crossp : 0u;
+            }
+        } else
         // store phase: whole band rows, ReLU (the bias is already in the
         // DC bin, so every pixel of every patch carries it)
         {
@@ -502,11 +561,11 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     }
 }
 
-template <int L, int TG, int NV>
-static hipError_t launch_inverse_band(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y,
-                                      hipStream_t s, const LaunchEvents& ev) {
+template <int L, int TG, int NV, bool POOL>
+static hipError_t launch_inverse_band_v(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y,
+                                        hipStream_t s, const LaunchEvents& ev) {
     constexpr int NT = TG * (L / 2);
-    auto kern = inverse_band_kernel<L, TG, NV>;
+    auto kern = inverse_band_kernel<L, TG, NV, POOL>;
     const int lds = p.inv_lds;
     if (lds > 64 * 1024) {
         const hipError_t attr = allow_dynamic_lds(kern, lds);
@@ -521,10 +580,18 @@ static hipError_t launch_inverse_band(const fftsplit_plan_s& p, const float2* ys
     const int nitems = ngroups * p.prob.cout;
     const int ipw = items_per_workgroup(nitems, p.cus * per_cu);
     const dim3 grid(unsigned((nitems + ipw - 1) / ipw));
-    const unsigned y_bytes = unsigned(size_t(p.prob.n) * p.prob.cout * p.prob.h * p.prob.w * 4);
+    const unsigned y_bytes = unsigned(size_t(p.prob.n) * p.prob.cout * (POOL ? (p.prob.h / 2) * (p.prob.w / 2)
+                                                                             : p.prob.h * p.prob.w) * 4);
     return launch_kernel(kern, grid, dim3(NT), unsigned(lds), s, ev.start, ev.stop, ys, bias, y, p.prob.cout, p.coutp,
                          p.prob.h, p.prob.w, p.T, p.th, p.tw, p.nt, p.ntp, ngroups, nitems, ipw, p.inv_obp,
                          int(p.relu), y_bytes, 1.0f / float(p.prob.h), 1.0f / float(p.tw), 1.0f / float(p.th));
+}
+
+template <int L, int TG, int NV>
+static hipError_t launch_inverse_band(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y,
+                                      hipStream_t s, const LaunchEvents& ev) {
+    return p.pool_fused ? launch_inverse_band_v<L, TG, NV, true>(p, ys, bias, y, s, ev)
+                        : launch_inverse_band_v<L, TG, NV, false>(p, ys, bias, y, s, ev);
 }
 
 template <int L, int TG, bool OAA>

@@ -2,6 +2,7 @@
 // split method.  One thread per output pixel; a wavefront's 64 outputs read
 // two rows of 128 consecutive inputs as float2 pairs when the width is even.
 #include "fftsplit_internal.hpp"
+#include "launch_util.hpp"
 
 namespace fftsplit {
 
@@ -19,12 +20,11 @@ __global__ __launch_bounds__(256) void maxpool_kernel(const float* __restrict__ 
     y[idx] = fmaxf(a, b);
 }
 
-hipError_t launch_maxpool(const float* x, float* y, int n, int c, int h, int w, hipStream_t s) {
+hipError_t launch_maxpool(const float* x, float* y, int n, int c, int h, int w, hipStream_t s, hipEvent_t stop) {
     const int ho = h / 2, wo = w / 2;
     const size_t total = size_t(n) * c * ho * wo;
     const unsigned blocks = unsigned((total + 255) / 256);
-    hipLaunchKernelGGL(maxpool_kernel, dim3(blocks), dim3(256), 0, s, x, y, h, w, ho, wo, total);
-    return hipGetLastError();
+    return launch_kernel(maxpool_kernel, dim3(blocks), dim3(256), 0, s, nullptr, stop, x, y, h, w, ho, wo, total);
 }
 
 }  // namespace fftsplit

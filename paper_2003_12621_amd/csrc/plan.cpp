@@ -157,7 +157,7 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     if (p.n <= 0 || p.cin <= 0 || p.h <= 0 || p.w <= 0 || p.cout <= 0 || p.k <= 0)
         return fail(FFTSPLIT_ERROR_INVALID_VALUE, "all dimensions must be positive");
     if (p.tile < 0) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "tile must be >= 0 (0 = choose)");
-    const unsigned known = FFTSPLIT_OVERLAP_ADD | FFTSPLIT_BIAS | FFTSPLIT_RELU;
+    const unsigned known = FFTSPLIT_OVERLAP_ADD | FFTSPLIT_BIAS | FFTSPLIT_RELU | FFTSPLIT_MAXPOOL;
     if (p.flags & ~known) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "unknown flag bits");
     if (p.k % 2 == 0) return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "kernel size must be odd");
     if (p.stride != 1) return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "only stride 1 is supported");
@@ -168,6 +168,8 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     if (p.cin > 65535 || p.cout > 65535)
         return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "channel counts above 65535 are not supported");
     const bool oaa = (p.flags & FFTSPLIT_OVERLAP_ADD) != 0;
+    const bool pool = (p.flags & FFTSPLIT_MAXPOOL) != 0;
+    if (pool && (p.h < 2 || p.w < 2)) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "max-pool needs h, w >= 2");
 
     int tile = p.tile;
     if (tile == 0) {
@@ -264,6 +266,7 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     plan->oaa = oaa;
     plan->bias = (p.flags & FFTSPLIT_BIAS) != 0;
     plan->relu = (p.flags & FFTSPLIT_RELU) != 0;
+    plan->pool = pool;
     plan->wspec_bytes = wsb;
     plan->xspec_off = 0;
     plan->xspec_bytes = xs;
@@ -307,6 +310,17 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
 
     choose_forward_band(*plan);
     choose_inverse_band(*plan);
+    // The max-pool goes into the band inverse's store phase when its slots
+    // pair up into pooled rows (even tile size, even image height);
+    // otherwise the unpooled output is staged in the workspace.
+    plan->pool_fused = pool && plan->inv_band && g.T % 2 == 0 && p.h % 2 == 0;
+    plan->pre_off = plan->ws_bytes;
+    plan->pre_bytes = 0;
+    if (pool && !plan->pool_fused) {
+        plan->pre_off = round_up(plan->ws_bytes, 256);
+        plan->pre_bytes = size_t(p.n) * p.cout * p.h * p.w * 4;
+        plan->ws_bytes = plan->pre_off + plan->pre_bytes;
+    }
 
     const char* log = std::getenv("FFTSPLIT_LOG");
     if (log && *log && *log != '0') {

@@ -11,6 +11,10 @@ activation buffers are shared by all layers.
 With method="direct" the same stack runs on the library's spatial
 convolution (fftsplit_direct_conv2d), the method the paper compares
 against on these layers; the plans then serve only as layer descriptors.
+
+With fuse_pool (the default for the split method) the layers that end a
+stage carry FFTSPLIT_MAXPOOL, so their convolution writes the pooled
+activation directly and no separate pooling pass runs.
 """
 from __future__ import annotations
 
@@ -23,7 +27,7 @@ POOL_AFTER = (2, 4, 7, 10, 13)
 
 class VGG16Stack:
     def __init__(self, layers: Sequence, batch: int, hw: int = 224, tiles: Optional[Sequence[int]] = None,
-                 mode: str = "os", device=None, method: str = "split"):
+                 mode: str = "os", device=None, method: str = "split", fuse_pool: bool = True):
         """`layers`: 13 (w, b) pairs (torch CUDA float32 tensors or arrays);
         `tiles`: optional per-layer tile sizes (0 or None = plan's choice)."""
         import torch
@@ -32,6 +36,7 @@ class VGG16Stack:
         if method not in ("split", "direct"):
             raise ValueError("method must be 'split' or 'direct'")
         self.method = method
+        self.fuse_pool = fuse_pool and method == "split"
         dev = torch.device("cuda", torch.cuda.current_device() if device is None else int(device))
         self.device = dev
         self.batch = batch
@@ -45,7 +50,8 @@ class VGG16Stack:
             b = torch.as_tensor(b, dtype=torch.float32, device=dev).contiguous()
             cout, cin, k, _ = w.shape
             t = 0 if tiles is None or not tiles[i - 1] else int(tiles[i - 1])
-            plan = Plan(batch, cin, s, s, cout, k, tile=t, mode=mode, bias=True, relu=True, device=dev.index)
+            plan = Plan(batch, cin, s, s, cout, k, tile=t, mode=mode, bias=True, relu=True, device=dev.index,
+                        pool=self.fuse_pool and i in POOL_AFTER)
             self.plans.append(plan)
             self.wspecs.append(plan.transform_weights(w) if method == "split" else plan.direct_transform_weights(w))
             self.biases.append(b)
@@ -65,20 +71,22 @@ class VGG16Stack:
         """Runs the stack on x [batch, 3, hw, hw].  Returns the final
         activation [batch, 512, hw/32, hw/32] (a view of an internal buffer),
         or with keep=True also a list of copies of every layer's post-ReLU
-        output (before pooling)."""
+        output (before pooling; needs fuse_pool=False)."""
+        if keep and self.fuse_pool:
+            raise ValueError("keep=True needs the unpooled outputs: build the stack with fuse_pool=False")
         cur, other = self._buf
         a = x
         outs = []
         for i, plan in enumerate(self.plans, start=1):
-            shape = (plan.n, plan.cout, plan.h, plan.w)
-            y = other[: plan.n * plan.cout * plan.h * plan.w].view(shape)
+            shape = plan.out_shape
+            y = other[: plan.n * plan.cout * shape[2] * shape[3]].view(shape)
             if self.method == "split":
                 plan.conv2d(a, self.wspecs[i - 1], self.biases[i - 1], out=y, workspace=self.workspace)
             else:
                 plan.direct_conv2d(a, self.wspecs[i - 1], self.biases[i - 1], out=y)
             if keep:
                 outs.append(y.clone())
-            if i in POOL_AFTER:
+            if i in POOL_AFTER and not plan.pool:
                 pooled = cur[: plan.n * plan.cout * (plan.h // 2) * (plan.w // 2)].view(
                     plan.n, plan.cout, plan.h // 2, plan.w // 2)
                 a = maxpool2x2(y, out=pooled)

@@ -191,3 +191,30 @@ def test_overlap_add_is_deterministic():
     xd = _dev(x)
     outs = [plan.conv2d(xd, wspec).cpu().numpy() for _ in range(3)]
     assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
+
+
+POOL_CASES = [
+    # (n, cin, h, w, cout, k), tile, mode: which path pools
+    ((2, 5, 28, 28, 9, 3), 14, "os"),     # band inverse, pooled in its store phase
+    ((3, 4, 56, 56, 70, 5), 28, "os"),    # band, items spanning images
+    ((1, 3, 60, 40, 6, 3), 6, "os"),      # band, T/2 odd and items starting mid tile-row: straddles
+    ((2, 3, 26, 44, 5, 3), 14, "os"),     # band, ragged last tile rows and columns
+    ((1, 2, 27, 28, 4, 3), 14, "os"),     # odd height: staged output + pooling pass
+    ((1, 3, 30, 30, 5, 3), 14, "oaa"),    # overlap-add: staged output + pooling pass
+    ((2, 3, 17, 19, 4, 3), 3, "oaa"),     # OaAConv configuration, odd sizes
+]
+
+
+@pytest.mark.parametrize("shape,tile,mode", POOL_CASES, ids=[f"{s}-T{t}-{m}" for s, t, m in POOL_CASES])
+@pytest.mark.parametrize("relu", [False, True])
+def test_fused_maxpool(shape, tile, mode, relu):
+    n, cin, h, w, cout, k = shape
+    print(f"[case] maxpool {shape} T={tile} {mode} relu={relu}", flush=True)
+    x, wt = small_layer(n, cin, h, w, cout, k, seed=77)
+    b = make_random_bias(cout, cin, k, seed=78)
+    plan = fs.Plan(n, cin, h, w, cout, k, tile=tile, mode=mode, bias=True, relu=relu, pool=True)
+    y = plan.conv2d(_dev(x), plan.transform_weights(_dev(wt)), _dev(b))
+    torch.cuda.synchronize()
+    assert tuple(y.shape) == (n, cout, h // 2, w // 2)
+    ref = oracle.maxpool2x2(oracle.direct_xcorr2d(x, wt, b, relu=relu))
+    assert rel_l2(y.cpu().numpy(), ref) <= GATE

@@ -27,7 +27,7 @@ SAMPLE = [0, 1]
 def vgg_run():
     from paper_2003_12621_amd.vgg import VGG16Stack, POOL_AFTER
     x, layers = make_vgg16(batch=32, seed=0)
-    stack = VGG16Stack(layers, batch=32)
+    stack = VGG16Stack(layers, batch=32, fuse_pool=False)
     out, outs = stack.forward(torch.from_numpy(x).cuda(), keep=True)
     torch.cuda.synchronize()
     print(f"[vgg] tiles per layer: {stack.tiles}", flush=True)
@@ -77,3 +77,18 @@ def test_vgg16_direct_stack_matches_oracle(vgg_ref):
     err = rel_l2(out.cpu().numpy(), vgg_ref[1])
     print(f"[vgg] direct stack final rel_l2 = {err:.3e}", flush=True)
     assert err <= 1e-4
+
+
+def test_vgg16_fused_pool_stack(vgg_run, vgg_ref):
+    """The stack as it runs by default: the stage-ending layers write pooled
+    activations (FFTSPLIT_MAXPOOL); same final output as with separate
+    pooling passes, bit for bit, and within the gate of the oracle chain."""
+    from paper_2003_12621_amd.vgg import VGG16Stack
+    x, layers, _, final_unfused, _ = vgg_run
+    stack = VGG16Stack(layers, batch=32)
+    assert [p.pool for p in stack.plans] == [i in (2, 4, 7, 10, 13) for i in range(1, 14)]
+    out = stack.forward(torch.from_numpy(x).cuda())
+    torch.cuda.synchronize()
+    got = out[SAMPLE].cpu().numpy()
+    np.testing.assert_array_equal(got, final_unfused)
+    assert rel_l2(got, vgg_ref[1]) <= 1e-4
