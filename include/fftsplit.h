@@ -142,6 +142,12 @@ typedef struct {
      * FFTSPLIT_CONTRACT_TILE=[g3:|g4:]MxNxK overrides it at plan time. */
     int contract_tile_m, contract_tile_n, contract_stage_k, contract_real_products;
     int spec_group;      /* G of the output-spectra layout */
+    /* 1 if fftsplit_conv2d sums the input channels inside the inverse stage
+     * (layers of at most 4 input channels at L = 8, 3 at L = 16, on the
+     * overlap-save band path): no contraction launch, and the output
+     * spectra region of the workspace is left untouched.  The stage entry
+     * points are unaffected. */
+    int fused_channel_sum;
     /* Bytes of the filter layout of the direct (spatial) convolution,
      * fftsplit_direct_transform_weights. */
     size_t direct_wspec_bytes;

@@ -53,7 +53,8 @@ class PlanInfo(ctypes.Structure):
                 ("aux_offset", ctypes.c_size_t), ("aux_bytes", ctypes.c_size_t),
                 ("contract_tile_m", ctypes.c_int), ("contract_tile_n", ctypes.c_int),
                 ("contract_stage_k", ctypes.c_int), ("contract_real_products", ctypes.c_int),
-                ("spec_group", ctypes.c_int), ("direct_wspec_bytes", ctypes.c_size_t)]
+                ("spec_group", ctypes.c_int), ("fused_channel_sum", ctypes.c_int),
+                ("direct_wspec_bytes", ctypes.c_size_t)]
 
 
 class FftsplitError(RuntimeError):

@@ -81,14 +81,20 @@ size_t y_bytes(fftsplit_plan_t p) {
 // The inverse stage into y: with FFTSPLIT_MAXPOOL either pooled in the
 // inverse kernel itself or through the workspace's unpooled staging buffer
 // and a pooling pass.
+// xs/ws non-NULL: the fused variant (fuse_cin) that sums the channels itself.
 hipError_t launch_inverse_to_y(fftsplit_plan_t plan, const float2* ys, const float* bias, float* y, void* workspace,
-                               hipStream_t stream, const LaunchEvents& ev) {
+                               hipStream_t stream, const LaunchEvents& ev, const float2* xs = nullptr,
+                               const float2* ws = nullptr) {
     void* aux = plan->aux_bytes ? ws_at(workspace, plan->aux_off) : nullptr;
-    if (!plan->pool || plan->pool_fused) return launch_inverse(*plan, ys, bias, y, aux, stream, ev);
+    auto inverse = [&](float* out, const LaunchEvents& e) {
+        return xs ? launch_inverse_fused(*plan, xs, ws, bias, out, stream, e)
+                  : launch_inverse(*plan, ys, bias, out, aux, stream, e);
+    };
+    if (!plan->pool || plan->pool_fused) return inverse(y, ev);
     float* pre = reinterpret_cast<float*>(ws_at(workspace, plan->pre_off));
     LaunchEvents first;
     first.start = ev.start;
-    const hipError_t e = launch_inverse(*plan, ys, bias, pre, aux, stream, first);
+    const hipError_t e = inverse(pre, first);
     if (e != hipSuccess) return e;
     return launch_maxpool(pre, y, plan->prob.n, plan->prob.cout, plan->prob.h, plan->prob.w, stream, ev.stop);
 }
@@ -180,6 +186,10 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_conv2d(fftsplit_plan_t plan, const fl
     last.stop = t_events.stop;
     if (fftsplit_status_t s = launched(launch_forward(*plan, x, xs, stream, first), "forward patch transform launch"))
         return s;
+    if (plan->fuse_cin)
+        return launched(launch_inverse_to_y(plan, ys, bias, y, workspace, stream, last, xs,
+                                            static_cast<const float2*>(wspec)),
+                        "inverse patch transform launch");
     if (fftsplit_status_t s = launched(launch_contract(*plan, xs, static_cast<const float2*>(wspec), ys, stream, middle),
                                        "contraction launch"))
         return s;

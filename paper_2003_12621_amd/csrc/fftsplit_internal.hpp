@@ -39,6 +39,10 @@ struct fftsplit_plan_s {
     // workspace at pre_off and a pooling pass follows
     bool pool_fused;
     size_t pre_off, pre_bytes;
+    // inputs of at most 4 (L = 8) or 3 (L = 16) channels (overlap-save,
+    // band inverse):
+    // conv2d sums the channels inside the inverse and skips the contraction
+    bool fuse_cin;
 };
 
 namespace fftsplit {
@@ -127,6 +131,10 @@ hipError_t launch_oaa_forward(const fftsplit_plan_s& p, const float* x, float2* 
                               const LaunchEvents& ev);
 hipError_t launch_oaa_inverse(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y, float* aux,
                               hipStream_t s, const LaunchEvents& ev);
+// the band inverse with the per-bin channel sum for plans with fuse_cin:
+// reads the patch spectra xs and the filter spectra ws, not output spectra
+hipError_t launch_inverse_fused(const fftsplit_plan_s& p, const float2* xs, const float2* ws, const float* bias,
+                                float* y, hipStream_t s, const LaunchEvents& ev);
 // overlap-add seams from the per-patch L x L results in aux (k_inverse.hip)
 hipError_t launch_seam(const fftsplit_plan_s& p, const float* aux, const float* bias, float* y, hipStream_t s,
                        hipEvent_t stop);

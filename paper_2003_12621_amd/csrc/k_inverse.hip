@@ -271,11 +271,21 @@ __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux
 //     in the first and last tile row of an item only the columns of its own
 //     tiles are written;
 //   * LDS strides are odd, so the lanes of a wave spread over the banks.
-template <int L, int TG, int NV, bool POOL>
+// POOL: the 2x2 max-pool happens in the store phase (FFTSPLIT_MAXPOOL).
+// NCI > 0 (layers with NCI <= 4 input channels): the per-bin channel sum
+// (eq. 9) is done here instead of by the contraction, and the output
+// spectra are never stored: each item forms its spectra from the patch
+// spectra xsp (held in registers while consecutive items share the patch
+// group: items run patch-group-major, so the group's NCI channels are read
+// once per workgroup) and the item's filter spectra, staged in LDS from
+// wsp.  The products are the contraction's (the two packed slots part by
+// part).
+template <int L, int TG, int NV, bool POOL, int NCI>
 __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     const float2* __restrict__ ys, const float* __restrict__ bias, float* __restrict__ y, int cout, int coutp, int h,
     int w, int T, int th, int tw, int nt, int ntp, int ngroups, int nitems, int ipw, int obp, int relu,
-    unsigned y_bytes, float inv_h, float inv_tw, float inv_th) {
+    unsigned y_bytes, float inv_h, float inv_tw, float inv_th, const float2* __restrict__ xsp,
+    const float2* __restrict__ wsp, int cin, int wl_off) {
     constexpr int H2 = L / 2, NT = TG * H2, NW = NT / 64, TP = H2 + 1;
     constexpr int TTS = band_half_stride(L);  // half-spectrum patch stride (float2), odd
     constexpr int F = stored_bins(L);
@@ -298,6 +308,18 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     const int lw = xcd_logical_block(blockIdx.x, gridDim.x);
     const int ibeg = lw * ipw;
     const int iend = min(ibeg + ipw, nitems);
+    // (channel, first patch) of an item: channel-major, or patch-group-major
+    // when the channel sum is done here
+    auto decode = [&](int item, int& co, int& t0) {
+        if constexpr (NCI > 0) {
+            const int gi = item / cout;
+            co = item - gi * cout;
+            t0 = gi * TG;
+        } else {
+            co = item / ngroups;
+            t0 = (item - co * ngroups) * TG;
+        }
+    };
 
     // column-pass roles: patch uc (fastest across lanes), column j
     const int uc = tid % TG;
@@ -309,13 +331,48 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     // two slots of their real bins, pa[k1] and pb[k1] (k1 >= 1) their
     // complex bins k1.
     float2 pa[H2], pb[H2];
+    // slot of pa[k1] / pb[k1] in this lane's column
+    auto slot_a = [&](int k1) { return j0 ? (k1 == 0 ? bin_real_a(L) : bin_col0(L, k1)) : bin_mid(L, k1, jc); };
+    auto slot_b = [&](int k1) { return j0 ? (k1 == 0 ? bin_real_b(L) : bin_colh(L, k1)) : bin_mid(L, k1 + H2, jc); };
+    // NCI > 0: patch spectra of this lane's column for the current patch
+    // group, and the next item's filter spectra (WPT per thread)
+    constexpr int WPT = NCI > 0 ? (F * NCI + NT - 1) / NT : 1;
+    float2 xa[NCI > 0 ? NCI : 1][H2], xb[NCI > 0 ? NCI : 1][H2];
+    float2 wpre[WPT];
+    float2* wl = reinterpret_cast<float2*>(lds_raw) + wl_off;
+    int gcur = -1;
+    const BufRsrc rxs = make_rsrc(xsp, NCI > 0 ? unsigned(size_t(kChanBlock) * ntp * 8 * F) : 0u);
+    const BufRsrc rws = make_rsrc(wsp, NCI > 0 ? unsigned(size_t(F) * cin * coutp * 8) : 0u);
+    auto load_x = [&](int t0) {
+        // channel c < 16 of bin f: ((f * 16 + c) * ntp + t) * 8 bytes
+        const unsigned lane8 = unsigned(t0 + opaque(uc)) * 8u;
+        const unsigned fs8 = unsigned(kChanBlock) * unsigned(ntp) * 8u;
+#pragma unroll
+        for (int ci = 0; ci < (NCI > 0 ? NCI : 1); ++ci) {
+#pragma unroll
+            for (int k1 = 0; k1 < H2; ++k1) {
+                xa[ci][k1] = buf_load_f32x2(rxs, lane8 + unsigned(slot_a(k1)) * fs8, unsigned(ci * ntp * 8));
+                xb[ci][k1] = buf_load_f32x2(rxs, lane8 + unsigned(slot_b(k1)) * fs8, unsigned(ci * ntp * 8));
+            }
+        }
+    };
     auto load_spectra = [&](int item) {
         int co = 0, t0 = 0;
         bool ok = false;
         if (item >= 0) {
-            co = item / ngroups;
-            t0 = (item - co * ngroups) * TG;
+            decode(item, co, t0);
             ok = true;
+        }
+        if constexpr (NCI > 0) {
+            // W[f][ci][co] of the item's channel, e = f * NCI + ci
+#pragma unroll
+            for (int k = 0; k < WPT; ++k) {
+                const int e = k * NT + tid;
+                const int f = e / NCI, ci = e - (e / NCI) * NCI;
+                const bool in = ok && e < F * NCI;
+                wpre[k] = buf_load_f32x2(rws, in ? unsigned(((f * cin + ci) * coutp + co) * 8) : kOutOfRange, 0);
+            }
+            return;
         }
         // item = co * ngroups + t0 / TG: the item's run starts at item * F * TG
         const unsigned lane8 = unsigned(yspec_offset(co, 0, t0 + opaque(uc), F, TG, ngroups)) * 8u;
@@ -343,9 +400,40 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     const int dq = slot_step / h, dr = slot_step - dq * h;
 
     auto process = [&](int item) {
-        const int co = item / ngroups;
-        const int t0 = (item - co * ngroups) * TG;
+        int co, t0;
+        decode(item, co, t0);
         const BandGeom g = band_geom(t0, TG, nt, h, T, 0, th, tw);
+        if constexpr (NCI > 0) {
+            // the item's filter spectra into LDS, the next item's loaded,
+            // the patch group's spectra loaded when the group changes
+#pragma unroll
+            for (int k = 0; k < WPT; ++k)
+                if (k * NT + tid < F * NCI) wl[k * NT + tid] = wpre[k];
+            if (t0 != gcur) {
+                load_x(t0);
+                gcur = t0;
+            }
+            __syncthreads();
+            // per-bin channel sum (eq. 9): pa, pb = sum_ci W x
+            auto cmul = [](float2 a, float2 b) { return make_float2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x); };
+            auto pmul = [](float2 a, float2 b) { return make_float2(a.x * b.x, a.y * b.y); };
+#pragma unroll
+            for (int k1 = 0; k1 < H2; ++k1) {
+                float2 sa = make_float2(0.f, 0.f), sb = make_float2(0.f, 0.f);
+                const float2* wa = wl + slot_a(k1) * NCI;
+                const float2* wb = wl + slot_b(k1) * NCI;
+#pragma unroll
+                for (int ci = 0; ci < NCI; ++ci) {
+                    // the two packed slots (lane 0, k1 = 0) multiply part by part
+                    const float2 pa_ = (k1 == 0 && j0) ? pmul(wa[ci], xa[ci][k1]) : cmul(wa[ci], xa[ci][k1]);
+                    const float2 pb_ = (k1 == 0 && j0) ? pmul(wb[ci], xb[ci][k1]) : cmul(wb[ci], xb[ci][k1]);
+                    sa = make_float2(sa.x + pa_.x, sa.y + pa_.y);
+                    sb = make_float2(sb.x + pb_.x, sb.y + pb_.y);
+                }
+                pa[k1] = sa;
+                pb[k1] = sb;
+            }
+        }
 
         // column pass
         {
@@ -561,12 +649,14 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     }
 }
 
-template <int L, int TG, int NV, bool POOL>
+template <int L, int TG, int NV, bool POOL, int NCI = 0>
 static hipError_t launch_inverse_band_v(const fftsplit_plan_s& p, const float2* ys, const float* bias, float* y,
-                                        hipStream_t s, const LaunchEvents& ev) {
+                                        hipStream_t s, const LaunchEvents& ev, const float2* xs = nullptr,
+                                        const float2* ws = nullptr) {
     constexpr int NT = TG * (L / 2);
-    auto kern = inverse_band_kernel<L, TG, NV, POOL>;
-    const int lds = p.inv_lds;
+    auto kern = inverse_band_kernel<L, TG, NV, POOL, NCI>;
+    const int wl_off = (p.inv_lds + 15) / 16 * 2;   // float2 offset of the filter-spectrum stage
+    const int lds = NCI > 0 ? (wl_off + stored_bins(L) * NCI) * 8 : p.inv_lds;
     if (lds > 64 * 1024) {
         const hipError_t attr = allow_dynamic_lds(kern, lds);
         if (attr != hipSuccess) return attr;
@@ -584,7 +674,8 @@ static hipError_t launch_inverse_band_v(const fftsplit_plan_s& p, const float2* 
                                                                              : p.prob.h * p.prob.w) * 4);
     return launch_kernel(kern, grid, dim3(NT), unsigned(lds), s, ev.start, ev.stop, ys, bias, y, p.prob.cout, p.coutp,
                          p.prob.h, p.prob.w, p.T, p.th, p.tw, p.nt, p.ntp, ngroups, nitems, ipw, p.inv_obp,
-                         int(p.relu), y_bytes, 1.0f / float(p.prob.h), 1.0f / float(p.tw), 1.0f / float(p.th));
+                         int(p.relu), y_bytes, 1.0f / float(p.prob.h), 1.0f / float(p.tw), 1.0f / float(p.th), xs,
+                         ws, p.prob.cin, wl_off);
 }
 
 template <int L, int TG, int NV>
@@ -592,6 +683,34 @@ static hipError_t launch_inverse_band(const fftsplit_plan_s& p, const float2* ys
                                       hipStream_t s, const LaunchEvents& ev) {
     return p.pool_fused ? launch_inverse_band_v<L, TG, NV, true>(p, ys, bias, y, s, ev)
                         : launch_inverse_band_v<L, TG, NV, false>(p, ys, bias, y, s, ev);
+}
+
+template <int L, int TG, int NV, bool POOL>
+static hipError_t launch_inverse_fused_p(const fftsplit_plan_s& p, const float2* xs, const float2* ws,
+                                         const float* bias, float* y, hipStream_t s, const LaunchEvents& ev) {
+    switch (p.prob.cin) {
+        case 1: return launch_inverse_band_v<L, TG, NV, POOL, 1>(p, nullptr, bias, y, s, ev, xs, ws);
+        case 2: return launch_inverse_band_v<L, TG, NV, POOL, 2>(p, nullptr, bias, y, s, ev, xs, ws);
+        case 3: return launch_inverse_band_v<L, TG, NV, POOL, 3>(p, nullptr, bias, y, s, ev, xs, ws);
+        case 4:
+            if constexpr (L == 8) return launch_inverse_band_v<L, TG, NV, POOL, 4>(p, nullptr, bias, y, s, ev, xs, ws);
+            break;
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_inverse_fused(const fftsplit_plan_s& p, const float2* xs, const float2* ws, const float* bias,
+                                float* y, hipStream_t s, const LaunchEvents& ev) {
+    if (!p.fuse_cin) return hipErrorInvalidValue;
+    switch (p.L) {
+        case 8:
+            return p.pool_fused ? launch_inverse_fused_p<8, 64, kBandNV8, true>(p, xs, ws, bias, y, s, ev)
+                                : launch_inverse_fused_p<8, 64, kBandNV8, false>(p, xs, ws, bias, y, s, ev);
+        case 16:
+            return p.pool_fused ? launch_inverse_fused_p<16, 32, kBandNV16, true>(p, xs, ws, bias, y, s, ev)
+                                : launch_inverse_fused_p<16, 32, kBandNV16, false>(p, xs, ws, bias, y, s, ev);
+    }
+    return hipErrorInvalidValue;
 }
 
 template <int L, int TG, bool OAA>

@@ -314,6 +314,13 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     // pair up into pooled rows (even tile size, even image height);
     // otherwise the unpooled output is staged in the workspace.
     plan->pool_fused = pool && plan->inv_band && g.T % 2 == 0 && p.h % 2 == 0;
+    // Layers with at most 4 (L = 8) or 3 (L = 16) input channels, whose
+    // patch spectra fit the inverse's registers: the channel sum moves into
+    // the inverse (no contraction launch, output spectra never stored).
+    // FFTSPLIT_FUSE_CIN=0 turns it off.
+    plan->fuse_cin = plan->inv_band && p.cin <= (g.L == 8 ? 4 : (g.L == 16 ? 3 : 0));
+    if (const char* e = std::getenv("FFTSPLIT_FUSE_CIN"))
+        if (*e == '0') plan->fuse_cin = false;
     plan->pre_off = plan->ws_bytes;
     plan->pre_bytes = 0;
     if (pool && !plan->pool_fused) {
@@ -378,6 +385,7 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_plan_info(fftsplit_plan_t plan, fftsp
     i.contract_real_products = plan->con_products;
     i.direct_wspec_bytes = direct_wspec_bytes(*plan);
     i.spec_group = patch_group(plan->L);
+    i.fused_channel_sum = plan->fuse_cin ? 1 : 0;
     *out = i;
     return FFTSPLIT_SUCCESS;
 }

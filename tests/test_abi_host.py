@@ -205,3 +205,16 @@ def test_spectra_layout_helpers_roundtrip():
         np.testing.assert_allclose(stored_to_full(st, L), full, rtol=0, atol=1e-12)
     # the error measure sees imaginary parts
     assert rel_l2(np.array([1 + 1j]), np.array([1 + 0j])) == 1.0
+
+
+@pytest.mark.parametrize("cin,tile,fused", [(3, 6, 1), (4, 6, 1), (5, 6, 0), (3, 14, 1), (4, 14, 0), (3, 30, 0)])
+def test_fused_channel_sum_choice(cin, tile, fused):
+    """Tiny-Cin layers sum their channels in the inverse (registers allow 4
+    at L = 8, 3 at L = 16, none at L = 32); overlap-add never does."""
+    assert plan(n=2, cin=cin, h=56, w=56, cout=16, k=3, tile=tile).info.fused_channel_sum == fused
+    assert plan(n=2, cin=cin, h=56, w=56, cout=16, k=3, tile=tile, mode="oaa").info.fused_channel_sum == 0
+
+
+def test_fused_channel_sum_env_off(monkeypatch):
+    monkeypatch.setenv("FFTSPLIT_FUSE_CIN", "0")
+    assert plan(n=2, cin=3, h=56, w=56, cout=16, k=3, tile=6).info.fused_channel_sum == 0

@@ -218,3 +218,37 @@ def test_fused_maxpool(shape, tile, mode, relu):
     assert tuple(y.shape) == (n, cout, h // 2, w // 2)
     ref = oracle.maxpool2x2(oracle.direct_xcorr2d(x, wt, b, relu=relu))
     assert rel_l2(y.cpu().numpy(), ref) <= GATE
+
+
+FUSED_CIN_CASES = [
+    # (n, cin, h, w, cout, k), tile, pool
+    ((2, 3, 56, 56, 20, 3), 14, False),    # L = 16, three channels (an RGB input)
+    ((1, 1, 40, 44, 70, 3), 14, True),     # L = 16, one channel, pooled
+    ((3, 2, 30, 28, 9, 5), 4, False),      # L = 8, K = 5
+    ((2, 4, 24, 36, 66, 3), 6, True),      # L = 8, four channels, pooled
+    ((4, 3, 28, 28, 16, 3), 6, False),     # L = 8, items of 64 patches spanning images
+]
+
+
+@pytest.mark.parametrize("shape,tile,pool", FUSED_CIN_CASES,
+                         ids=[f"{s}-T{t}-pool{int(p)}" for s, t, p in FUSED_CIN_CASES])
+def test_fused_channel_sum(shape, tile, pool, monkeypatch):
+    """conv2d with the channel sum inside the inverse against the oracle, and
+    against the same plan with the contraction (FFTSPLIT_FUSE_CIN=0)."""
+    n, cin, h, w, cout, k = shape
+    print(f"[case] fused channel sum {shape} T={tile} pool={pool}", flush=True)
+    x, wt = small_layer(n, cin, h, w, cout, k, seed=91)
+    b = make_random_bias(cout, cin, k, seed=92)
+    outs = []
+    for fuse in ("1", "0"):
+        monkeypatch.setenv("FFTSPLIT_FUSE_CIN", fuse)
+        plan = fs.Plan(n, cin, h, w, cout, k, tile=tile, bias=True, relu=True, pool=pool)
+        assert plan.info.fused_channel_sum == int(fuse)
+        y = plan.conv2d(_dev(x), plan.transform_weights(_dev(wt)), _dev(b))
+        torch.cuda.synchronize()
+        outs.append(y.cpu().numpy())
+    ref = oracle.direct_xcorr2d(x, wt, b, relu=True)
+    if pool:
+        ref = oracle.maxpool2x2(ref)
+    assert rel_l2(outs[0], ref) <= GATE
+    assert rel_l2(outs[0], outs[1]) <= 1e-6
