@@ -96,11 +96,23 @@ def cpu_baseline(layer, x, w, b, tile, budget_s=12.0):
         done += 1
     per_img = t_total / done
     gflops = layer.direct_flops / layer.n / per_img / 1e9
+    # the oracle's direct cross-correlation (eq. 1) on a smaller sample
+    d_done, d_total = 0, 0.0
+    while d_done < layer.n and d_total < budget_s / 3:
+        t0 = time.perf_counter()
+        oracle.direct_xcorr2d(x[d_done:d_done + 1], w, b)
+        d_total += time.perf_counter() - t0
+        d_done += 1
+    d_img = d_total / d_done
     return {"value": round(gflops, 3), "unit": "GFLOP/s", "cores": int(min(cores, blas_threads)),
             "kind": "oracle",
             "sample": f"oracle.split_conv (float64 numpy, naive-DFT split, overlap-save) on {done} of "
                       f"{layer.n} images, {t_total:.1f} s; {1.0 / per_img:.3f} images/s; "
-                      f"{cores} host cores visible, BLAS threads {blas_threads}"}
+                      f"{cores} host cores visible, BLAS threads {blas_threads}",
+            "direct_xcorr2d": {"value": round(layer.direct_flops / layer.n / d_img / 1e9, 3), "unit": "GFLOP/s",
+                               "sample": f"oracle.direct_xcorr2d (float64 numpy, K*K shifted tensordots) on "
+                                         f"{d_done} of {layer.n} images, {d_total:.1f} s; "
+                                         f"{1.0 / d_img:.3f} images/s"}}
 
 
 def load_traffic(kernel, workload_tag):
@@ -222,6 +234,7 @@ def main():
     ap.add_argument("--mode", default="os", choices=["os", "oaa"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache stage timings")
     ap.add_argument("--no-compare", action="store_true",
                     help="skip timing the spatial methods (this library's direct kernel, torch/MIOpen conv2d)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
@@ -312,6 +325,37 @@ def main():
     ms_per_step_staged = evs[0][0].elapsed_time(evs[-1][5]) / args.steps
     avg = lambda v: sum(v) / len(v)  # noqa: E731
 
+    # Cold-cache stage times: before every stage a 512 MB buffer is read
+    # (summed), which fills the 256 MB last-level cache with clean lines, so
+    # each stage reads its inputs from HBM (the timings above are warm: a
+    # stage may find its input there).
+    cold = None
+    if not args.no_cold:
+        flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)   # 512 MB
+        ncold = min(args.steps, 20)
+        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(ncold)]
+        for row in cev:
+            for e in row:
+                e.record()
+        torch.cuda.synchronize()
+        for i in range(ncold):
+            ev = cev[i]
+            flush.sum()
+            fs.set_timing_events(ev[0], ev[1])
+            plan.forward(xd, ws)
+            fs.set_timing_events()
+            flush.sum()
+            fs.set_timing_events(ev[2], ev[3])
+            plan.contract(wspec, ws)
+            fs.set_timing_events()
+            flush.sum()
+            fs.set_timing_events(ev[4], ev[5])
+            plan.inverse(ws, bias=bd, out=y)
+            fs.set_timing_events()
+        torch.cuda.synchronize()
+        cold = [avg([e[2 * j].elapsed_time(e[2 * j + 1]) for e in cev]) for j in range(3)]
+        del flush
+
     counts = algorithmic_counts(layer, info)
     fwd_gbs = counts["forward_bytes"] / (avg(fwd) * 1e-3) / 1e9
     inv_gbs = counts["inverse_bytes"] / (avg(inv) * 1e-3) / 1e9
@@ -369,6 +413,14 @@ def main():
                         "frac_hbm": round(inv_gbs / HBM_PEAK_GBS, 4), "bytes": counts["inverse_bytes"],
                         "traffic": load_traffic("inverse", wtag)},
         },
+        "stages_cold": None if cold is None else {
+            "forward": {"ms": round(cold[0], 4), "frac_hbm": round(counts["forward_bytes"] / (cold[0] * 1e-3) / 1e9
+                                                                 / HBM_PEAK_GBS, 4)},
+            "contract": {"ms": round(cold[1], 4), "frac_mfma": round(counts["contract_flops"] / (cold[1] * 1e-3)
+                                                                     / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4)},
+            "inverse": {"ms": round(cold[2], 4), "frac_hbm": round(counts["inverse_bytes"] / (cold[2] * 1e-3) / 1e9
+                                                                 / HBM_PEAK_GBS, 4)},
+            "note": "each stage after a 512 MB read has replaced the last-level cache's contents"},
         "timing": "ms_per_step: K fftsplit_conv2d calls between two events on the launch stream, after "
                   "a warm-up that lets the clocks settle; stage times: K further steps as three stage calls "
                   "with each kernel's start/stop taken from its dispatch timestamps (hipExtLaunchKernel events)",
