@@ -132,6 +132,8 @@ def test_arch_only_plan_cannot_launch():
     assert st == fs.ERROR_INVALID_VALUE
     assert "architecture name only" in fs.last_error()
     assert L.fftsplit_forward(p._h, fake, fake, 1 << 30, None) == fs.ERROR_INVALID_VALUE
+    assert L.fftsplit_direct_conv2d(p._h, fake, fake, None, fake, None) == fs.ERROR_INVALID_VALUE
+    assert L.fftsplit_direct_transform_weights(p._h, fake, fake, None) == fs.ERROR_INVALID_VALUE
 
 
 def test_auto_tile_choice_and_env_override(monkeypatch):
@@ -218,3 +220,16 @@ def test_fused_channel_sum_choice(cin, tile, fused):
 def test_fused_channel_sum_env_off(monkeypatch):
     monkeypatch.setenv("FFTSPLIT_FUSE_CIN", "0")
     assert plan(n=2, cin=3, h=56, w=56, cout=16, k=3, tile=6).info.fused_channel_sum == 0
+
+
+def test_maxpool_flag():
+    """FFTSPLIT_MAXPOOL halves the output (floor); it needs a 2 x 2 image."""
+    p = plan(n=2, cin=8, h=28, w=28, cout=8, k=3, tile=14, pool=True)
+    assert p.out_shape == (2, 8, 14, 14)
+    assert plan(n=1, cin=2, h=27, w=29, cout=3, k=3, tile=14, pool=True).out_shape == (1, 3, 13, 14)
+    assert status_of(n=1, cin=2, h=1, w=8, cout=3, k=3, tile=6, pool=True) == fs.ERROR_INVALID_VALUE
+    # a plan that cannot pool inside the inverse stages the unpooled output
+    # in its workspace: odd height needs n*cout*h*w*4 more bytes
+    a = plan(n=1, cin=2, h=28, w=28, cout=3, k=3, tile=14).info.workspace_bytes
+    b = plan(n=1, cin=2, h=27, w=28, cout=3, k=3, tile=14, pool=True).info.workspace_bytes
+    assert b >= a + 1 * 3 * 27 * 28 * 4 - 4096
