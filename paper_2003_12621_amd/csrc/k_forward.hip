@@ -335,7 +335,10 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
         // the next item's loads stay in flight through this item's transforms
         load_band(item + 1 < iend ? item + 1 : -1);
 
-        // row pass (j fastest across lanes): rows 2j, 2j+1 of patch u's window
+        // row pass (j fastest across lanes): rows j and j + L/2 of patch u's
+        // window (rows a stride of L/2 apart, not adjacent ones, so that with
+        // the odd band pitch and half-spectrum row stride the 16 lanes of a
+        // patch spread over all banks)
         {
             const int j = tid % H2;
             const int u = tid / H2;
@@ -348,10 +351,10 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
                 const int a = tr - img * th;
                 // the band's rows run through the images in order: image row
                 // r of image img0 + sg sits at slot sg * h + r - r0
-                const int r = a * T - P + 2 * j;
+                const int r = a * T - P + j;
                 const int sb = __umul24(img - g.img0, h) - g.r0 + r;
                 s0 = unsigned(r) < unsigned(h) ? sb : zslot;
-                s1 = unsigned(r + 1) < unsigned(h) ? sb + 1 : zslot;
+                s1 = unsigned(r + H2) < unsigned(h) ? sb + H2 : zslot;
                 cb = co + b * T - P;
             }
             const float* r0 = band + s0 * bp + cb;
@@ -361,13 +364,13 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
             for (int qq = 0; qq < L; ++qq) z[qq] = make_float2(r0[qq], r1[qq]);
             __syncthreads();  // the half-spectrum buffer reuses the band's LDS
             fft<L, false>(z);
-            float2* ra = tb + opaque(u * TTS + 2 * j * TP);
+            float2* ra = tb + opaque(u * TTS + j * TP);
 #pragma unroll
             for (int k = 0; k <= H2; ++k) {
                 float2 a, b;
                 split_two_real(z[k], z[(L - k) % L], a, b);
                 ra[k] = a;
-                ra[TP + k] = b;
+                ra[H2 * TP + k] = b;
             }
         }
         __syncthreads();

@@ -473,13 +473,15 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
         }
         __syncthreads();
 
-        // row pass (j fastest across lanes) and placement of the crop in the band
+        // row pass (j fastest across lanes): rows j and j + L/2 (a stride of
+        // L/2 rows, so that the 16 lanes of a patch spread over all banks),
+        // and placement of the crop in the band
         {
             const int j = tid % H2;
             const int u = tid / H2;
             float2 z[L];
-            const float2* ra = tb + opaque(u * TTS + 2 * j * TP);
-            const float2* rb = ra + TP;
+            const float2* ra = tb + opaque(u * TTS + j * TP);
+            const float2* rb = ra + H2 * TP;
 #pragma unroll
             for (int k2 = 0; k2 < L; ++k2) {
                 if (k2 <= H2) {
@@ -493,23 +495,23 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
             __syncthreads();  // the output band reuses the half-spectrum LDS
             fft<L, true>(z);
             const int t = t0 + u;
-            if (t < nt && 2 * j < T) {
+            if (t < nt && j < T) {
                 const int tr = div_small(t, tw, inv_tw);
                 const int b = t - tr * tw;
                 const int img = div_small(tr, th, inv_th);
                 const int a = tr - img * th;
-                const int r = a * T + 2 * j;
+                const int r = a * T + j;
                 // rows run through the images in order: row r of image
                 // img0 + sg sits at slot sg * h + r - r0
                 const int sl = __umul24(img - g.img0, h) - g.r0 + r;
                 const bool ok0 = r < h;
-                const bool ok1 = r + 1 < h && 2 * j + 1 < T;
+                const bool ok1 = r + H2 < h && j + H2 < T;
                 float* d = ob + opaque(sl * obp + b * T);
 #pragma unroll
                 for (int q = 0; q < L; ++q) {
                     if (q < T) {
                         if (ok0) d[q] = z[q].x;
-                        if (ok1) d[obp + q] = z[q].y;
+                        if (ok1) d[H2 * obp + q] = z[q].y;
                     }
                 }
             }
