@@ -50,6 +50,11 @@ namespace fftsplit {
 // Granularity of the contraction's output tiles (patches x channels).
 constexpr int kTileGranule = 64;
 constexpr int kCoutGranule = 64;
+// Patches are padded to 64, or to 32 where the transforms' patch groups
+// allow it (L = 16, 32) and the output channels fill 128-wide tiles: the
+// contraction then runs 128 x 32 tiles, which halves the padding of layers
+// with few patches (a 14 x 14 image at T = 14 is one patch).
+constexpr int kTileGranuleSmall = 32;
 
 // Patches per work item of the forward/inverse transforms (L/2 threads
 // each), by FFT size; the odd sizes of the OaAConv configuration transform

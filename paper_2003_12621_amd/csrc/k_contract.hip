@@ -265,6 +265,7 @@ hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xs, const flo
             case 64064016: return launch_contract_v<64, 64, 16, 2, true>(p, xs, ws, ys, s, ev);
             case 128064016: return launch_contract_v<128, 64, 16, 2, true>(p, xs, ws, ys, s, ev);
             case 64128016: return launch_contract_v<64, 128, 16, 2, true>(p, xs, ws, ys, s, ev);
+            case 128032016: return launch_contract_v<128, 32, 16, 4, true>(p, xs, ws, ys, s, ev);
         }
     } else {
         switch (v) {
@@ -275,6 +276,7 @@ hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xs, const flo
             case 64128016: return launch_contract_v<64, 128, 16, 2>(p, xs, ws, ys, s, ev);
             case 128128016: return launch_contract_v<128, 128, 16, 2>(p, xs, ws, ys, s, ev);
             case 256064016: return launch_contract_v<256, 64, 16, 4>(p, xs, ws, ys, s, ev);
+            case 128032016: return launch_contract_v<128, 32, 16, 4>(p, xs, ws, ys, s, ev);
         }
     }
     return hipErrorInvalidValue;

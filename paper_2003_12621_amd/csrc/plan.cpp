@@ -56,9 +56,10 @@ static Geometry geometry(const fftsplit_problem_t& p, int L) {
     g.tw = (p.w + g.T - 1) / g.T;
     const double nt = double(p.n) * g.th * g.tw;
     g.nt = nt > INT_MAX ? -1 : int(nt);
-    g.ntp = g.nt < 0 ? -1 : int(round_up(size_t(g.nt), kTileGranule));
     g.bins = stored_bins(L);
     g.coutp = int(round_up(size_t(p.cout), kCoutGranule));
+    const bool small_granule = (L == 16 || L == 32) && g.coutp % 128 == 0;
+    g.ntp = g.nt < 0 ? -1 : int(round_up(size_t(g.nt), small_granule ? kTileGranuleSmall : kTileGranule));
     const double F = g.bins, ntp = double(g.ntp), cin = p.cin, coutp = g.coutp;
     const double img = double(p.n) * p.h * p.w;
     const double fwd = 4.0 * img * cin + 8.0 * F * cin * ntp;
@@ -204,7 +205,7 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     }
     if (oaa && g.T < p.k - 1)
         return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "overlap-add needs tile >= k - 1");
-    if (g.nt < 0 || g.ntp < 0 || g.ntp / kTileGranule > INT_MAX / 2)
+    if (g.nt < 0 || g.ntp < 0 || g.ntp / kTileGranuleSmall > INT_MAX / 2)
         return fail(FFTSPLIT_ERROR_INVALID_VALUE, "too many patches");
     // The overlap-add seam buffer is indexed with 32-bit offsets.
     if (oaa && size_t(p.cout) * size_t(g.ntp) * size_t(g.L) * size_t(g.L) > size_t(INT_MAX))
@@ -277,11 +278,12 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     plan->aux_bytes = oaa ? size_t(p.cout) * size_t(g.ntp) * size_t(g.L) * size_t(g.L) * 4 : 0;
     plan->ws_bytes = plan->aux_off + plan->aux_bytes;
 
-    // Contraction variant: 64x64 tiles, 16-channel stages, three real
-    // products per complex multiply-add (fastest measured on every layer
-    // shape); FFTSPLIT_CONTRACT_TILE=[g3:|g4:]BMxBNxKC overrides.
-    plan->con_bm = 64;
-    plan->con_bn = 64;
+    // Contraction variant: 64x64 tiles (128x32 where the patches are padded
+    // to 32 only), 16-channel stages, three real products per complex
+    // multiply-add (fastest measured on every layer shape);
+    // FFTSPLIT_CONTRACT_TILE=[g3:|g4:]BMxBNxKC overrides.
+    plan->con_bm = g.ntp % 64 == 0 ? 64 : 128;
+    plan->con_bn = g.ntp % 64 == 0 ? 64 : 32;
     plan->con_kc = 16;
     plan->con_products = 3;
     if (const char* v = std::getenv("FFTSPLIT_CONTRACT_TILE")) {

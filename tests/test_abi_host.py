@@ -233,3 +233,16 @@ def test_maxpool_flag():
     a = plan(n=1, cin=2, h=28, w=28, cout=3, k=3, tile=14).info.workspace_bytes
     b = plan(n=1, cin=2, h=27, w=28, cout=3, k=3, tile=14, pool=True).info.workspace_bytes
     assert b >= a + 1 * 3 * 27 * 28 * 4 - 4096
+
+
+def test_small_patch_granule():
+    """Few patches and output channels in 128s: patches padded to 32 and the
+    contraction in 128 x 32 tiles; otherwise 64 and 64 x 64."""
+    i = plan(n=32, cin=512, h=14, w=14, cout=512, k=3, tile=14).info
+    assert (i.tiles, i.tiles_padded, i.contract_tile_m, i.contract_tile_n) == (32, 32, 128, 32)
+    i = plan(n=32, cin=512, h=14, w=14, cout=64, k=3, tile=14).info      # channels not in 128s
+    assert (i.tiles_padded, i.contract_tile_m, i.contract_tile_n) == (64, 64, 64)
+    i = plan(n=8, cin=64, h=14, w=14, cout=128, k=3, tile=6).info        # L = 8 groups 64 patches
+    assert i.tiles_padded % 64 == 0 and i.contract_tile_n == 64
+    i = plan(n=16, cin=8, h=56, w=56, cout=256, k=5, tile=28).info       # 64 patches: unchanged
+    assert (i.tiles_padded, i.contract_tile_m, i.contract_tile_n) == (64, 64, 64)

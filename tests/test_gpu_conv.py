@@ -75,6 +75,9 @@ EDGE = [
     ((1, 4, 20, 20, 6, 1), 16),    # K = 1 (pointwise), L = 16
     ((2, 3, 30, 30, 4, 7), 26),    # K = 7 at L = 32
     ((1, 130, 17, 17, 3, 3), 14),  # Cin not a multiple of the contraction's K step
+    ((32, 16, 14, 14, 128, 3), 14),  # one patch per image: patches padded to 32, 128x32 tiles
+    ((3, 20, 28, 28, 256, 3), 14),   # 12 patches padded to 32
+    ((5, 8, 40, 40, 130, 3), 30),    # output channels not in 128s: padded to 64
 ]
 
 
