@@ -255,3 +255,44 @@ def test_fused_channel_sum(shape, tile, pool, monkeypatch):
         ref = oracle.maxpool2x2(ref)
     assert rel_l2(outs[0], ref) <= GATE
     assert rel_l2(outs[0], outs[1]) <= 1e-6
+
+
+def test_streams_and_concurrent_plans():
+    """Launches go to the caller's current stream: two layers on two
+    streams, each with its own workspace, give the results they give alone."""
+    x1, w1 = small_layer(2, 16, 40, 40, 32, 3, seed=101)
+    x2, w2 = small_layer(4, 8, 28, 36, 24, 5, seed=102)
+    p1 = fs.Plan(2, 16, 40, 40, 32, 3, tile=14)
+    p2 = fs.Plan(4, 8, 28, 36, 24, 5, tile=12)
+    ws1, ws2 = p1.transform_weights(_dev(w1)), p2.transform_weights(_dev(w2))
+    xd1, xd2 = _dev(x1), _dev(x2)
+    ref1 = p1.conv2d(xd1, ws1).clone()
+    ref2 = p2.conv2d(xd2, ws2).clone()
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = []
+    for _ in range(3):
+        with torch.cuda.stream(s1):
+            y1 = p1.conv2d(xd1, ws1)
+        with torch.cuda.stream(s2):
+            y2 = p2.conv2d(xd2, ws2)
+        outs.append((y1, y2))
+    torch.cuda.synchronize()
+    for y1, y2 in outs:
+        assert torch.equal(y1, ref1) and torch.equal(y2, ref2)
+    assert rel_l2(ref1.cpu().numpy(), oracle.direct_xcorr2d(x1, w1)) <= GATE
+    assert rel_l2(ref2.cpu().numpy(), oracle.direct_xcorr2d(x2, w2)) <= GATE
+
+
+def test_deterministic_output():
+    """Overlap-save results are bitwise reproducible run to run (no atomics;
+    every sum in a fixed order); overlap-add's seam sums too."""
+    x, w = small_layer(3, 20, 33, 35, 40, 5, seed=103)
+    for mode in ("os", "oaa"):
+        plan = fs.Plan(3, 20, 33, 35, 40, 5, tile=12, mode=mode)
+        wspec = plan.transform_weights(_dev(w))
+        xd = _dev(x)
+        a = plan.conv2d(xd, wspec).clone()
+        b = plan.conv2d(xd, wspec).clone()
+        torch.cuda.synchronize()
+        assert torch.equal(a, b), mode
