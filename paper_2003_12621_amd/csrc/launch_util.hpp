@@ -91,14 +91,6 @@ __device__ __forceinline__ void buf_store_f32x2(float2 v, BufRsrc r, unsigned vo
     __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(int2v, v), r, voff, soff, 0);
 }
 
-// Waits until every vector memory operation this wave has issued is done.
-// Placed where a loop's prefetched loads are consumed, so that the
-// stores issued afterwards never make a later wait include them.
-__device__ __forceinline__ void wait_vmem_all() {
-    // s_waitcnt vmcnt(0), expcnt and lgkmcnt left at their no-wait maximum
-    __builtin_amdgcn_s_waitcnt(0x0F70);
-}
-
 // Optional timing events of one entry-point call: `start` is recorded when
 // the call's first kernel begins and `stop` when its last kernel ends
 // (hipExtLaunchKernel timestamps, no separate event packets).
