@@ -157,7 +157,12 @@ typedef struct {
  * Queries the device: its gcnArchName must start with "gfx950", else
  * FFTSPLIT_ERROR_ARCH.  With prob->tile == 0 the plan picks T from a cost
  * model over L = 8, 16, 32; the environment variable FFTSPLIT_TILE forces a
- * tile size.  No device memory is touched.  *out is set only on success. */
+ * tile size.  No device memory is touched.  *out is set only on success.
+ * Other environment variables read here (for experiments; the defaults are
+ * the measured best): FFTSPLIT_CONTRACT_TILE (see contract_tile_m),
+ * FFTSPLIT_FORWARD_BAND=0 / FFTSPLIT_INVERSE_BAND=0 (general forward /
+ * inverse kernels instead of the row-band ones), FFTSPLIT_FUSE_CIN=0 (no
+ * channel sum in the inverse), FFTSPLIT_LOG=1 (print the plan to stderr). */
 fftsplit_status_t fftsplit_plan(const fftsplit_problem_t* prob, int device, fftsplit_plan_t* out);
 
 /* As fftsplit_plan, but for a named architecture string (host-only, no HIP
