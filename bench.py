@@ -156,9 +156,29 @@ def bench_vgg16(args):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
     flops = 0
-    s = 224
     for i, (cin, cout, hw) in enumerate(VGG16_LAYERS, start=1):
         flops += 2 * VGG_BATCH * cout * hw * hw * cin * 9
+    # per-layer times: further passes with each layer's convolution call
+    # timed from its kernels' dispatch timestamps (max-pools included where
+    # a layer ends a stage)
+    reps = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(13)]
+            for _ in range(args.steps)]
+    for row in reps:
+        for a, b in row:
+            a.record()
+            b.record()
+    torch.cuda.synchronize()
+    for row in reps:
+        stack.forward(xd, layer_events=row)
+    torch.cuda.synchronize()
+    per_layer = []
+    for i, (cin, cout, hw) in enumerate(VGG16_LAYERS):
+        lms = sum(r[i][0].elapsed_time(r[i][1]) for r in reps) / len(reps)
+        plan = stack.plans[i]
+        per_layer.append({"layer": i + 1, "cin": cin, "cout": cout, "hw": hw, "tile": plan.tile,
+                          "pool": bool(plan.pool), "fused_channel_sum": bool(plan.info.fused_channel_sum),
+                          "ms": round(lms, 4),
+                          "GFLOP/s": round(2 * VGG_BATCH * cout * hw * hw * cin * 9 / (lms * 1e-3) / 1e9, 1)})
     spatial = None
     if not args.no_compare:
         spatial = time_vgg_spatial(args, layers, x, stack)
@@ -168,7 +188,7 @@ def bench_vgg16(args):
            "dtype": "f32", "data": "synthetic",
            "config": {"workload": f"vgg16 conv stack, batch {VGG_BATCH}, 3x224x224, bias+ReLU, 5 max-pools",
                       "tiles": stack.tiles, "mode": args.mode},
-           "images_per_s": round(VGG_BATCH / (ms * 1e-3), 1)}
+           "images_per_s": round(VGG_BATCH / (ms * 1e-3), 1), "layers": per_layer}
     if spatial is not None:
         for v in spatial.values():
             if isinstance(v, dict):

@@ -20,7 +20,7 @@ from __future__ import annotations
 
 from typing import List, Optional, Sequence
 
-from . import Plan, maxpool2x2
+from . import Plan, maxpool2x2, set_timing_events
 
 POOL_AFTER = (2, 4, 7, 10, 13)
 
@@ -67,11 +67,13 @@ class VGG16Stack:
     def tiles(self):
         return [p.tile for p in self.plans]
 
-    def forward(self, x, keep=False):
+    def forward(self, x, keep=False, layer_events=None):
         """Runs the stack on x [batch, 3, hw, hw].  Returns the final
         activation [batch, 512, hw/32, hw/32] (a view of an internal buffer),
         or with keep=True also a list of copies of every layer's post-ReLU
-        output (before pooling; needs fuse_pool=False)."""
+        output (before pooling; needs fuse_pool=False).  layer_events: 13
+        (start, stop) torch.cuda.Event pairs that time each layer's
+        convolution call from its kernels' dispatch timestamps."""
         if keep and self.fuse_pool:
             raise ValueError("keep=True needs the unpooled outputs: build the stack with fuse_pool=False")
         cur, other = self._buf
@@ -80,10 +82,14 @@ class VGG16Stack:
         for i, plan in enumerate(self.plans, start=1):
             shape = plan.out_shape
             y = other[: plan.n * plan.cout * shape[2] * shape[3]].view(shape)
+            if layer_events is not None:
+                set_timing_events(*layer_events[i - 1])
             if self.method == "split":
                 plan.conv2d(a, self.wspecs[i - 1], self.biases[i - 1], out=y, workspace=self.workspace)
             else:
                 plan.direct_conv2d(a, self.wspecs[i - 1], self.biases[i - 1], out=y)
+            if layer_events is not None:
+                set_timing_events()
             if keep:
                 outs.append(y.clone())
             if i in POOL_AFTER and not plan.pool:
