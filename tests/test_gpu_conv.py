@@ -296,3 +296,46 @@ def test_deterministic_output():
         b = plan.conv2d(xd, wspec).clone()
         torch.cuda.synchronize()
         assert torch.equal(a, b), mode
+
+
+def _random_cases(count=48, seed=2024):
+    """Seeded random layer shapes over the whole plan space: every kernel
+    size, every FFT size that fits, both placements, bias / ReLU / max-pool,
+    channel counts around the 16 / 64 / 128 granules."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < count:
+        k = int(rng.choice([1, 3, 5, 7]))
+        L = int(rng.choice([8, 16, 32]))
+        t = L - k + 1
+        mode = str(rng.choice(["os", "oaa"]))
+        if mode == "oaa" and t < k - 1:
+            continue
+        if rng.random() < 0.15 and k > 1:          # the OaAConv configuration
+            t, mode = k, "oaa"
+        n = int(rng.integers(1, 4))
+        h = int(rng.integers(1, 3 * t + 5))
+        w = int(rng.integers(1, 3 * t + 5))
+        if rng.random() < 0.5:
+            w = max(4, w - w % 4)                  # widths the row-band kernels take
+        cin = int(rng.choice([1, 2, 3, 4, 5, 16, 17, 33]))
+        cout = int(rng.choice([1, 3, 16, 64, 65, 128, 130]))
+        pool = bool(rng.random() < 0.25) and h >= 2 and w >= 2
+        cases.append(((n, cin, h, w, cout, k), t, mode, bool(rng.random() < 0.5), bool(rng.random() < 0.5), pool))
+    return cases
+
+
+@pytest.mark.parametrize("shape,tile,mode,bias,relu,pool", _random_cases(),
+                         ids=[f"{s}-T{t}-{m}-b{int(b)}r{int(r)}p{int(p)}" for s, t, m, b, r, p in _random_cases()])
+def test_random_layers(shape, tile, mode, bias, relu, pool):
+    n, cin, h, w, cout, k = shape
+    print(f"[case] random {shape} T={tile} {mode} bias={bias} relu={relu} pool={pool}", flush=True)
+    x, wt = small_layer(n, cin, h, w, cout, k, seed=sum(shape) + tile)
+    b = make_random_bias(cout, cin, k, seed=5) if bias else None
+    plan = fs.Plan(n, cin, h, w, cout, k, tile=tile, mode=mode, bias=bias, relu=relu, pool=pool)
+    y = plan.conv2d(_dev(x), plan.transform_weights(_dev(wt)), None if b is None else _dev(b))
+    torch.cuda.synchronize()
+    ref = oracle.direct_xcorr2d(x, wt, b, relu=relu)
+    if pool:
+        ref = oracle.maxpool2x2(ref)
+    assert rel_l2(y.cpu().numpy(), ref) <= GATE
