@@ -220,11 +220,13 @@ __global__ __launch_bounds__(TG * (L / 2)) void forward_kernel(const float* __re
 //     before item i is transformed, and item i's spectra are stored
 //     straight from the column pass, so loads, transforms and stores of
 //     neighbouring items overlap;
-//   * LDS banks (32 four-byte banks): the band pitch is odd, so the 16
-//     row-pass lanes of a patch, which read rows 2j, hit 16 distinct bank
-//     pairs; the patch stride of the half spectra is odd, so the row-pass
-//     writes and column-pass reads of a wave's patches spread evenly; the
-//     band is written with 4-byte stores (odd rows are not 8-byte aligned).
+//   * LDS banks (32 four-byte banks): the row pass pairs rows j and
+//     j + L/2 (not 2j and 2j+1); with the odd band pitch the L/2 row-pass
+//     lanes of a patch, which read rows j, hit distinct banks, and with the
+//     odd row stride of the half spectra (L/2+1 float2) its row writes do
+//     too; the patch stride of the half spectra is odd, so the column-pass
+//     reads of a wave's patches spread evenly; the band is written with
+//     4-byte stores (odd rows are not 8-byte aligned).
 template <int L, int TG, int NV>
 __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
     const float* __restrict__ x, float2* __restrict__ xs, int cin, int h, int w, int T, int P, int th, int tw, int nt,
