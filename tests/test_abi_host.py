@@ -246,3 +246,16 @@ def test_small_patch_granule():
     assert i.tiles_padded % 64 == 0 and i.contract_tile_n == 64
     i = plan(n=16, cin=8, h=56, w=56, cout=256, k=5, tile=28).info       # 64 patches: unchanged
     assert (i.tiles_padded, i.contract_tile_m, i.contract_tile_n) == (64, 64, 64)
+
+
+def test_size_limits():
+    """Largest problems the 32-bit offsets allow are accepted; beyond them
+    NOT_SUPPORTED (arch-only plans: nothing is allocated)."""
+    # 2.15 GB of patch spectra: accepted (above 2 GiB the general kernels run)
+    assert status_of(n=512, cin=256, h=56, w=56, cout=256, k=5, tile=28) == fs.SUCCESS
+    # patch spectra above 4 GiB
+    assert status_of(n=1100, cin=256, h=56, w=56, cout=256, k=5, tile=28) == fs.ERROR_NOT_SUPPORTED
+    # input tensor above 2^29 elements
+    assert status_of(n=700, cin=256, h=56, w=56, cout=16, k=5, tile=28) == fs.ERROR_NOT_SUPPORTED
+    # image plane above 2^31 pixels
+    assert status_of(n=1, cin=1, h=50000, w=50000, cout=1, k=3, tile=6) == fs.ERROR_NOT_SUPPORTED

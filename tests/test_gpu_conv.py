@@ -339,3 +339,27 @@ def test_random_layers(shape, tile, mode, bias, relu, pool):
     if pool:
         ref = oracle.maxpool2x2(ref)
     assert rel_l2(y.cpu().numpy(), ref) <= GATE
+
+
+def test_large_layer_general_kernels():
+    """512 x 256 x 56 x 56 -> 256, K = 5, T = 28: 2.15 GB of patch spectra,
+    past the 2 GiB the row-band kernels address, so the general forward and
+    inverse kernels run at full size; checked on sampled images and channels.
+    Inputs are drawn on the device from a seeded generator and the sampled
+    images copied to the host for the oracle."""
+    n, cin, h, w, cout, k = 512, 256, 56, 56, 256, 5
+    g = torch.Generator(device="cuda")
+    g.manual_seed(77)
+    xd = torch.relu(torch.randn((n, cin, h, w), generator=g, device="cuda"))
+    wd = torch.randn((cout, cin, k, k), generator=g, device="cuda") * float(np.sqrt(2.0 / (cin * k * k)))
+    plan = fs.Plan(n, cin, h, w, cout, k, tile=28)
+    assert plan.info.xspec_bytes >= 2 ** 31
+    y = plan.conv2d(xd, plan.transform_weights(wd))
+    torch.cuda.synchronize()
+    wt = wd.cpu().numpy()
+    sel = [3, 97, 200, 255]
+    for img in (0, 257, 511):
+        xi = xd[img:img + 1].cpu().numpy()
+        ref = oracle.direct_xcorr2d(xi, wt[sel])
+        got = y[img:img + 1, sel].cpu().numpy()
+        assert rel_l2(got, ref) <= GATE, img
