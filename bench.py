@@ -250,6 +250,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=None,
                     help=f"untimed steps first (default: as many as fill {WARMUP_S:g} s)")
     ap.add_argument("--config", default=DEFAULT_CONFIG, help="a layer config name, or vgg16")
+    ap.add_argument("--shape", default=None,
+                    help="any layer instead of a named config: n,cin,h,w,cout,k (ReLU(N(0,1)) inputs, He weights)")
     ap.add_argument("--tile", type=int, default=None)
     ap.add_argument("--mode", default="os", choices=["os", "oaa"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -270,18 +272,31 @@ def main():
     import paper_2003_12621_amd as fs
     from workloads import CONFIGS, make_config
 
-    if args.config == "vgg16":
+    if args.config == "vgg16" and not args.shape:
         return bench_vgg16(args)
-    cfg = CONFIGS[args.config]
-    layer = cfg["layer"]
-    tile = args.tile if args.tile is not None else (DEFAULT_TILE if args.config == DEFAULT_CONFIG else cfg["tiles"][-1])
+    if args.shape:
+        from workloads import Layer, make_layer
+        vals = [int(v) for v in args.shape.split(",")]
+        if len(vals) != 6:
+            raise SystemExit("--shape takes n,cin,h,w,cout,k")
+        layer = Layer(*vals)
+        args.config = "shape_" + "x".join(str(v) for v in vals)
+        tile = args.tile if args.tile is not None else 0
+        make = lambda: make_layer(layer)  # noqa: E731
+    else:
+        cfg = CONFIGS[args.config]
+        layer = cfg["layer"]
+        tile = (args.tile if args.tile is not None
+                else (DEFAULT_TILE if args.config == DEFAULT_CONFIG else cfg["tiles"][-1]))
+        make = lambda: make_config(args.config)  # noqa: E731
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
 
-    x, w, b = make_config(args.config)
+    x, w, b = make()
     plan = fs.Plan(layer.n, layer.cin, layer.h, layer.w, layer.cout, layer.k, tile=tile, mode=args.mode,
                    bias=b is not None, device=0)
     info = plan.info
+    tile = info.tile
     xd = torch.from_numpy(x).to(dev)
     wd = torch.from_numpy(w).to(dev)
     bd = None if b is None else torch.from_numpy(b).to(dev)
