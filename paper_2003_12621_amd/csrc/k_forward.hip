@@ -366,11 +366,16 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
             for (int qq = 0; qq < L; ++qq) z[qq] = make_float2(r0[qq], r1[qq]);
             __syncthreads();  // the half-spectrum buffer reuses the band's LDS
             fft<L, false>(z);
+            // A real row's spectrum is real at k = 0 and k = L/2: those two
+            // values share slot 0 as (re, im), already the packed sequence
+            // (column 0 + i * column L/2) the column pass transforms there.
             float2* ra = tb + opaque(u * TTS + j * TP);
+            ra[0] = make_float2(z[0].x, z[H2].x);
+            ra[H2 * TP] = make_float2(z[0].y, z[H2].y);
 #pragma unroll
-            for (int k = 0; k <= H2; ++k) {
+            for (int k = 1; k < H2; ++k) {
                 float2 a, b;
-                split_two_real(z[k], z[(L - k) % L], a, b);
+                split_two_real(z[k], z[L - k], a, b);
                 ra[k] = a;
                 ra[H2 * TP + k] = b;
             }
@@ -379,25 +384,20 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
 
         // column pass (patch index fastest across lanes).  Lane j >= 1
         // transforms column k2 = j; lane j = 0 the two real columns k2 = 0
-        // and k2 = L/2 packed as one complex sequence (column 0 + i * column
-        // L/2).  Both kinds of lane run one instruction stream -- packing and
-        // separating the two real spectra are selects -- so no wave executes
-        // two paths.  Each bin goes to (c, f, t0 + u): the TG lanes of
-        // consecutive patches write one contiguous 8*TG-byte segment.
+        // and k2 = L/2, which the row pass left packed in slot 0 as one
+        // complex sequence (column 0 + i * column L/2).  Both kinds of lane
+        // run one instruction stream -- separating the two real spectra is
+        // a select -- so no wave executes two paths.  Each bin goes to
+        // (c, f, t0 + u): the TG lanes of consecutive patches write one
+        // contiguous 8*TG-byte segment.
         {
             const int u = tid % TG;
             const int j = tid / TG;
             const bool j0 = j == 0;
-            const float2* cbuf = tb + opaque(u * TTS);
-            const float2* ca = cbuf + j;
-            const float2* chh = cbuf + H2;
-            const float m0 = j0 ? 1.f : 0.f;
+            const float2* ca = tb + opaque(u * TTS) + j;
             float2 cz[L];
 #pragma unroll
-            for (int m = 0; m < L; ++m) {
-                const float2 av = ca[m * TP];
-                cz[m] = make_float2(av.x, fmaf(m0, chh[m * TP].x, av.y));
-            }
+            for (int m = 0; m < L; ++m) cz[m] = ca[m * TP];
             __syncthreads();  // the next item's band reuses the half-spectrum LDS
             fft<L, false>(cz);
             // Lane j >= 1 stores bins (k1, j) and (k1 + L/2, j); lane 0 the

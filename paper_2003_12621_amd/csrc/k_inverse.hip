@@ -257,7 +257,7 @@ __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux
 
 
 // Overlap-save inverse transform writing whole row bands (width a multiple
-// of 4, at most 256).  Same work items and transforms as inverse_kernel;
+// of 4, at most 256; crop width T >= L/2).  Same work items and transforms as inverse_kernel;
 // what changes is the memory traffic and how items overlap:
 //   * the output spectra of item i+1 are loaded into registers while item
 //     i is transformed and stored;
@@ -302,6 +302,11 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     const unsigned bs8 = unsigned(TG) * 8u;   // bin stride (patch-group-major)
     auto opaque = [](int v) {
         asm volatile("" : "+v"(v));
+        return v;
+    };
+    // a uniform value the compiler may not hoist out of the item loop
+    auto opaque_s = [](int v) {
+        asm volatile("" : "+s"(v));
         return v;
     };
 
@@ -464,12 +469,11 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
             // the next item's spectra stay in flight through this item
             load_spectra(item + 1 < iend ? item + 1 : -1);
             fft<L, true>(cz);
+            // lane 0's result is the two real columns packed (column 0 +
+            // i * column L/2): it stays packed in slot 0 for the row pass
             float2* cbw = tb + opaque(uc * TTS);
 #pragma unroll
-            for (int m = 0; m < L; ++m) {
-                cbw[m * TP + jc] = j0 ? make_float2(cz[m].x, 0.f) : cz[m];
-                if (j0) cbw[m * TP + H2] = make_float2(cz[m].y, 0.f);
-            }
+            for (int m = 0; m < L; ++m) cbw[m * TP + jc] = cz[m];
         }
         __syncthreads();
 
@@ -482,18 +486,32 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
             float2 z[L];
             const float2* ra = tb + opaque(u * TTS + j * TP);
             const float2* rb = ra + H2 * TP;
+            // slot 0 holds (column 0, column L/2), both real in a row: the
+            // packed row sequence takes row j's value as its real part and
+            // row j + L/2's as its imaginary part
+            const float2 p0 = ra[0], q0 = rb[0];
+            z[0] = make_float2(p0.x, q0.x);
+            z[H2] = make_float2(p0.y, q0.y);
 #pragma unroll
-            for (int k2 = 0; k2 < L; ++k2) {
-                if (k2 <= H2) {
+            for (int k2 = 1; k2 < L; ++k2) {
+                if (k2 < H2) {
                     const float2 a = ra[k2], b = rb[k2];
                     z[k2] = make_float2(a.x - b.y, a.y + b.x);
-                } else {
+                } else if (k2 > H2) {
                     const float2 a = ra[L - k2], b = rb[L - k2];
                     z[k2] = make_float2(a.x + b.y, b.x - a.y);
                 }
             }
             __syncthreads();  // the output band reuses the half-spectrum LDS
             fft<L, true>(z);
+            // ReLU here, on values the transform has just computed, not in
+            // the store phase (where values read back from LDS would each
+            // need a NaN quieting before the max); with the max-pool the
+            // order does not matter: relu(max(.)) = max(relu(.))
+            if (relu) {
+#pragma unroll
+                for (int q = 0; q < L; ++q) z[q] = make_float2(fmaxf(z[q].x, 0.f), fmaxf(z[q].y, 0.f));
+            }
             const int t = t0 + u;
             if (t < nt && j < T) {
                 const int tr = div_small(t, tw, inv_tw);
@@ -506,12 +524,23 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
                 const int sl = __umul24(img - g.img0, h) - g.r0 + r;
                 const bool ok0 = r < h;
                 const bool ok1 = r + H2 < h && j + H2 < T;
+                // one exec-mask branch per row, and the crop width T (at
+                // least L/2) as a scalar loop bound re-read per item, so the
+                // tail's bound checks stay scalar compares
                 float* d = ob + opaque(sl * obp + b * T);
+                const int tq = opaque_s(T);
+                if (ok0) {
 #pragma unroll
-                for (int q = 0; q < L; ++q) {
-                    if (q < T) {
-                        if (ok0) d[q] = z[q].x;
-                        if (ok1) d[H2 * obp + q] = z[q].y;
+                    for (int q = 0; q < L; ++q) {
+                        if (q >= H2 && q >= tq) break;
+                        d[q] = z[q].x;
+                    }
+                }
+                if (ok1) {
+#pragma unroll
+                    for (int q = 0; q < L; ++q) {
+                        if (q >= H2 && q >= tq) break;
+                        d[H2 * obp + q] = z[q].y;
                     }
                 }
             }
@@ -542,43 +571,80 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
             const unsigned crossp = unsigned(cout - 1) * unsigned(hp) * unsigned(wp) * 4u;
             const int dqp = slot_step / hp, drp = slot_step - dqp * hp;
             const int sl0 = opaque(slot0);
+            // the lane writes whole pairs at pooled slots [sbeg, send): the
+            // first (last) tile row's slots only where its columns lie in
+            // the item's range; one unsigned compare per slot
+            const int sbeg = in_first ? 0 : rows_first;
+            const int send = lane_ok ? (in_last ? pslots : min(last0, pslots)) : 0;
+            const unsigned span = unsigned(max(send - sbeg, 0));
+            const int xs0 = sl0 - sbeg;
             const int x0 = sl0 + (g.r0 >> 1);
-            int qd = div_small(x0, hp, 2.f * inv_h);
-            int rr = x0 - qd * hp;
-            unsigned voff = unsigned((((g.img0 * cout + co) * hp + (g.r0 >> 1)) * wp) * 4) + unsigned(sl0 * wp * 4) +
-                            unsigned(8 * c4) + unsigned(qd) * crossp;
+            const int qd = div_small(x0, hp, 2.f * inv_h);
+            const int rr0 = x0 - qd * hp;
+            const unsigned voff0 = unsigned((((g.img0 * cout + co) * hp + (g.r0 >> 1)) * wp) * 4) +
+                                   unsigned(sl0 * wp * 4) + unsigned(8 * c4) + unsigned(qd) * crossp;
             const unsigned dq_off = unsigned(dqp) * crossp;
             const float* src = ob + 2 * sl0 * obp + 4 * c4;
+            auto pool4 = [&](const float* sp) {
+                return make_float2(fmaxf(fmaxf(sp[0], sp[1]), fmaxf(sp[obp], sp[obp + 1])),
+                                   fmaxf(fmaxf(sp[2], sp[3]), fmaxf(sp[obp + 2], sp[obp + 3])));
+            };
+            {
+                // batches of SB pooled slots, LDS reads before stores
+                constexpr int SB = 4, NP = (NV + 1) / 2;
+                int rr = rr0;
+                unsigned voff = voff0;
 #pragma unroll
-            for (int k = 0; k < (NV + 1) / 2; ++k) {
-                const int ps = sl0 + k * slot_step;
-                const bool ok = lane_ok && ps < pslots;
-                const bool first = ps < rows_first;
-                const bool last = ps >= last0;
-                const bool full = ok && (first ? in_first : (last ? in_last : true));
-                const float* sp = ok ? src + 2 * k * slot_step * obp : ob;
-                float2 v = make_float2(fmaxf(fmaxf(sp[0], sp[1]), fmaxf(sp[obp], sp[obp + 1])),
-                                       fmaxf(fmaxf(sp[2], sp[3]), fmaxf(sp[obp + 2], sp[obp + 3])));
-                if (relu) v = make_float2(fmaxf(v.x, 0.f), fmaxf(v.y, 0.f));
-                const unsigned soff = unsigned(k * slot_step * wp * 4);
-                buf_store_f32x2(v, ryo, full ? voff : kOutOfRange, soff);
-                if (edge) {
-                    const int lo = first ? lo0 : 0;
-                    const int hi = first ? hi_first : (last ? hi_last : wp);
-                    if (ok && !full && col + 2 > lo && col < hi) {
-                        buf_store_f32(v.x, ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
-                        buf_store_f32(v.y, ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
+                for (int k0 = 0; k0 < NP; k0 += SB) {
+                    float2 v[SB];
+                    bool full[SB];
+#pragma unroll
+                    for (int i = 0; i < SB && k0 + i < NP; ++i) {
+                        const int k = k0 + i;
+                        full[i] = unsigned(xs0 + k * slot_step) < span;
+                        v[i] = pool4(full[i] ? src + 2 * k * slot_step * obp : ob);
+                    }
+#pragma unroll
+                    for (int i = 0; i < SB && k0 + i < NP; ++i) {
+                        const int k = k0 + i;
+                        buf_store_f32x2(v[i], ryo, full[i] ? voff : kOutOfRange, unsigned(k * slot_step * wp * 4));
+                        rr += drp;
+                        voff += dq_off;
+                        const bool carry = rr >= hp;
+                        rr -= carry ? hp : 0;
+                        voff += carry ? crossp : 0u;
                     }
                 }
-                rr += drp;
-                voff += dq_off;
-                const bool carry = rr >= hp;
-                rr -= carry ? hp : 0;
-                voff += carry ? crossp : 0u;
+            }
+            if (edge) {
+                // pairs that straddle the item's first or last column
+                int rr = rr0;
+                unsigned voff = voff0;
+#pragma unroll
+                for (int k = 0; k < (NV + 1) / 2; ++k) {
+                    const int ps = sl0 + k * slot_step;
+                    const bool full = unsigned(xs0 + k * slot_step) < span;
+                    const bool first = ps < rows_first;
+                    const bool last = ps >= last0;
+                    const int lo = first ? lo0 : 0;
+                    const int hi = first ? hi_first : (last ? hi_last : wp);
+                    if (lane_ok && ps < pslots && !full && col + 2 > lo && col < hi) {
+                        const float2 ve = pool4(src + 2 * k * slot_step * obp);
+                        const unsigned soff = unsigned(k * slot_step * wp * 4);
+                        buf_store_f32(ve.x, ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
+                        buf_store_f32(ve.y, ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
+                    }
+                    rr += drp;
+                    voff += dq_off;
+                    const bool carry = rr >= hp;
+                    rr -= carry ? hp : 0;
+                    voff += carry ? crossp : 0u;
+                }
             }
         } else
-        // store phase: whole band rows, ReLU (the bias is already in the
-        // DC bin, so every pixel of every patch carries it)
+        // store phase: whole band rows (bias and ReLU are already applied:
+        // the bias is in the DC bin, so every pixel of every patch carries
+        // it, and ReLU came after the row transform)
         {
             const int tl = (t0 + TG < nt ? t0 + TG : nt) - 1;
             const int tr0 = t0 / tw, tr1 = tl / tw;
@@ -597,46 +663,86 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
             const bool in_last = col + 4 <= hi_last;
             const bool lane_ok = lrow < rpi;
             const int sl0 = opaque(slot0);
+            // the lane writes whole float4s at slots [sbeg, send): the first
+            // (last) tile row's slots only where its columns lie in the
+            // item's range; one unsigned compare per slot
+            const int sbeg = in_first ? 0 : rows_first;
+            const int send = lane_ok ? (in_last ? g.slots : min(last0, g.slots)) : 0;
+            const unsigned span = unsigned(max(send - sbeg, 0));
+            const int xs0 = sl0 - sbeg;
             const int x0 = sl0 + g.r0;
-            int qd = div_small(x0, h, inv_h);
-            int rr = x0 - qd * h;
-            unsigned voff = unsigned((((g.img0 * cout + co) * h + g.r0) * w) * 4) + unsigned(sl0 * w * 4) +
-                            unsigned(16 * c4) + unsigned(qd) * cross4;
+            const int qd = div_small(x0, h, inv_h);
+            const int rr0 = x0 - qd * h;
+            const unsigned voff0 = unsigned((((g.img0 * cout + co) * h + g.r0) * w) * 4) + unsigned(sl0 * w * 4) +
+                                   unsigned(16 * c4) + unsigned(qd) * cross4;
             const unsigned dq_off = unsigned(dq) * cross4;
             const float* src = ob + sl0 * obp + 4 * c4;
+            // Slot k of this lane goes to byte offset voff + k * slot_step *
+            // w * 4 of y, where voff advances by whole images (cross4) as the
+            // lane's rows cross into the next image.
+            //
             // Every lane issues one 16-byte store per slot (dropped through an
-            // out-of-range offset where it has nothing to write), so the count
-            // of stores after this item's spectrum loads is fixed; only where
-            // a float4 straddles an item's first or last column (never when
-            // items start and end on tile-row boundaries whose columns are
-            // multiples of 4) are four 4-byte stores added.
+            // out-of-range offset where it has nothing to write, after a read
+            // of the band's first float4), so the count of stores after this
+            // item's spectrum loads is fixed.  Slots go in batches of SB whose
+            // LDS reads are all issued before their stores (the compiler does
+            // not move LDS reads above buffer stores), so SB reads are in
+            // flight at once.
+            {
+                constexpr int SB = 4;
+                int rr = rr0;
+                unsigned voff = voff0;
 #pragma unroll
-            for (int k = 0; k < NV; ++k) {
-                const int sl = sl0 + k * slot_step;
-                const bool ok = lane_ok && sl < g.slots;
-                const bool first = sl < rows_first;
-                const bool last = sl >= last0;
-                const bool full = ok && (first ? in_first : (last ? in_last : true));
-                const float* sp = ok ? src + k * slot_step * obp : ob;
-                float4 v = make_float4(sp[0], sp[1], sp[2], sp[3]);
-                if (relu) v = make_float4(fmaxf(v.x, 0.f), fmaxf(v.y, 0.f), fmaxf(v.z, 0.f), fmaxf(v.w, 0.f));
-                const unsigned soff = unsigned(k * slot_step * w * 4);
-                buf_store_f32x4(v, ryo, full ? voff : kOutOfRange, soff);
-                if (edge) {
-                    const int lo = first ? lo0 : 0;
-                    const int hi = first ? hi_first : (last ? hi_last : w);
-                    if (ok && !full && col + 4 > lo && col < hi) {
-                        buf_store_f32(v.x, ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
-                        buf_store_f32(v.y, ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
-                        buf_store_f32(v.z, ryo, col + 2 >= lo && col + 2 < hi ? voff + 8u : kOutOfRange, soff);
-                        buf_store_f32(v.w, ryo, col + 3 >= lo && col + 3 < hi ? voff + 12u : kOutOfRange, soff);
+                for (int k0 = 0; k0 < NV; k0 += SB) {
+                    float4 v[SB];
+                    bool full[SB];
+#pragma unroll
+                    for (int i = 0; i < SB && k0 + i < NV; ++i) {
+                        const int k = k0 + i;
+                        full[i] = unsigned(xs0 + k * slot_step) < span;
+                        const float* sp = full[i] ? src + k * slot_step * obp : ob;
+                        v[i] = make_float4(sp[0], sp[1], sp[2], sp[3]);
+                    }
+#pragma unroll
+                    for (int i = 0; i < SB && k0 + i < NV; ++i) {
+                        const int k = k0 + i;
+                        buf_store_f32x4(v[i], ryo, full[i] ? voff : kOutOfRange, unsigned(k * slot_step * w * 4));
+                        rr += dr;
+                        voff += dq_off;
+                        const bool carry = rr >= h;
+                        rr -= carry ? h : 0;
+                        voff += carry ? cross4 : 0u;
                     }
                 }
-                rr += dr;
-                voff += dq_off;
-                const bool carry = rr >= h;
-                rr -= carry ? h : 0;
-                voff += carry ? cross4 : 0u;
+            }
+            // Only where a float4 straddles an item's first or last column
+            // (never when items start and end on tile-row boundaries whose
+            // columns are multiples of 4) are 4-byte stores added.
+            if (edge) {
+                int rr = rr0;
+                unsigned voff = voff0;
+#pragma unroll
+                for (int k = 0; k < NV; ++k) {
+                    const int sl = sl0 + k * slot_step;
+                    const bool full = unsigned(xs0 + k * slot_step) < span;
+                    const bool first = sl < rows_first;
+                    const bool last = sl >= last0;
+                    const int lo = first ? lo0 : 0;
+                    const int hi = first ? hi_first : (last ? hi_last : w);
+                    if (lane_ok && sl < g.slots && !full && col + 4 > lo && col < hi) {
+                        const float* se = src + k * slot_step * obp;
+                        const unsigned soff = unsigned(k * slot_step * w * 4);
+                        buf_store_f32(se[0], ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
+                        buf_store_f32(se[1], ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
+                        buf_store_f32(se[2], ryo, col + 2 >= lo && col + 2 < hi ? voff + 8u : kOutOfRange, soff);
+                        buf_store_f32(se[3], ryo, col + 3 >= lo && col + 3 < hi ? voff + 12u : kOutOfRange, soff);
+                    }
+                    rr += dr;
+                    voff += dq_off;
+                    const bool carry = rr >= h;
+                    rr -= carry ? h : 0;
+                    voff += carry ? cross4 : 0u;
+                }
             }
         }
         __syncthreads();  // the next item's column pass reuses the band's LDS

@@ -79,9 +79,17 @@ __device__ __forceinline__ float2 buf_load_f32x2(BufRsrc r, unsigned voff, unsig
 __device__ __forceinline__ float4 buf_load_f32x4(BufRsrc r, unsigned voff, unsigned soff) {
     return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
+// A store of more than 8 bytes needs one wait state before a VALU
+// instruction may overwrite its data registers.  The compiler's hazard model
+// assumes the wait is only needed when the scalar offset is not a register,
+// but on gfx950 a 16-byte store with a register scalar offset immediately
+// followed by such a write was measured to store the new value.  The
+// uniform offset is therefore added to the lane offset and the scalar
+// offset is the constant 0, for which the compiler inserts the wait.
+// (`soff` + an out-of-range `voff` stays out of range: both are below 2^31.)
 __device__ __forceinline__ void buf_store_f32x4(float4 v, BufRsrc r, unsigned voff, unsigned soff) {
     typedef int int4v __attribute__((ext_vector_type(4)));
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(int4v, v), r, voff, soff, 0);
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(int4v, v), r, voff + soff, 0, 0);
 }
 __device__ __forceinline__ void buf_store_f32(float v, BufRsrc r, unsigned voff, unsigned soff) {
     __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, voff, soff, 0);

@@ -80,13 +80,15 @@ static bool supported_L(int L) { return L == 8 || L == 16 || L == 32; }
 static bool oaaconv_L(int L, int k, bool oaa) { return oaa && L == 2 * k - 1 && (k == 3 || k == 5 || k == 7); }
 
 // The band variant of the inverse transform (overlap-save, width a multiple
-// of 4 and at most 256): used when the output band of any work item fits the
+// of 4 and at most 256, crop at least L/2 wide): used when the output band of any work item fits the
 // store slots it assigns and its LDS stays within two workgroups per compute
 // unit.  FFTSPLIT_INVERSE_BAND=0 turns it off.
 static void choose_inverse_band(fftsplit_plan_s& p) {
     p.inv_band = false;
     const int w = p.prob.w, L = p.L, T = p.T;
-    if (p.oaa || w % 4 != 0 || w > 256 || p.nt >= (1 << 22) || p.prob.h >= (1 << 22) ||
+    // (the row pass stores the first L/2 columns of a crop unconditionally,
+    // so the crop must be at least that wide: K <= L/2 + 1)
+    if (p.oaa || w % 4 != 0 || w > 256 || 2 * T < L || p.nt >= (1 << 22) || p.prob.h >= (1 << 22) ||
         p.yspec_bytes >= (size_t(1) << 31))
         return;
     if (const char* e = std::getenv("FFTSPLIT_INVERSE_BAND"))
