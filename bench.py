@@ -428,7 +428,7 @@ def main():
                    "tile": info.tile, "nfft": info.nfft, "mode": args.mode, "tiles": info.tiles,
                    "bins": info.bins,
                    "contract_variant": f"{info.contract_tile_m}x{info.contract_tile_n}x{info.contract_stage_k}"
-                                       f"/{info.contract_real_products}M"},
+                                       f"/{info.contract_real_products}M/prefetch{info.contract_prefetch}"},
         "images_per_s": round(layer.n / (ms_per_step * 1e-3), 1),
         "roofline": {"bound": "mfma", "kernel": "contract (per-bin complex Cin->Cout product)",
                      "achieved": round(con_tfs, 2), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",

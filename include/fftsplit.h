@@ -151,6 +151,11 @@ typedef struct {
     /* Bytes of the filter layout of the direct (spatial) convolution,
      * fftsplit_direct_transform_weights. */
     size_t direct_wspec_bytes;
+    /* Input-channel stages the contraction loads ahead of the one it
+     * multiplies: 1 (through registers) or 2 (straight into LDS, the
+     * default where the tile has that variant).  The environment variable
+     * FFTSPLIT_CONTRACT_PREFETCH=1..3 overrides it at plan time. */
+    int contract_prefetch;
 } fftsplit_plan_info_t;
 
 /* Validate `prob` (host) and create a plan for `device` (a HIP ordinal).
@@ -160,6 +165,7 @@ typedef struct {
  * tile size.  No device memory is touched.  *out is set only on success.
  * Other environment variables read here (for experiments; the defaults are
  * the measured best): FFTSPLIT_CONTRACT_TILE (see contract_tile_m),
+ * FFTSPLIT_CONTRACT_PREFETCH (see contract_prefetch),
  * FFTSPLIT_FORWARD_BAND=0 / FFTSPLIT_INVERSE_BAND=0 (general forward /
  * inverse kernels instead of the row-band ones), FFTSPLIT_FUSE_CIN=0 (no
  * channel sum in the inverse), FFTSPLIT_LOG=1 (print the plan to stderr). */

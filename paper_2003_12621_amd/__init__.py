@@ -54,7 +54,7 @@ class PlanInfo(ctypes.Structure):
                 ("contract_tile_m", ctypes.c_int), ("contract_tile_n", ctypes.c_int),
                 ("contract_stage_k", ctypes.c_int), ("contract_real_products", ctypes.c_int),
                 ("spec_group", ctypes.c_int), ("fused_channel_sum", ctypes.c_int),
-                ("direct_wspec_bytes", ctypes.c_size_t)]
+                ("direct_wspec_bytes", ctypes.c_size_t), ("contract_prefetch", ctypes.c_int)]
 
 
 class FftsplitError(RuntimeError):

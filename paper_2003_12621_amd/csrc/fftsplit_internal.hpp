@@ -23,8 +23,9 @@ struct fftsplit_plan_s {
     size_t xspec_off, xspec_bytes, yspec_off, yspec_bytes, aux_off, aux_bytes;
     size_t ws_bytes;
     // contraction kernel variant: tile BM x BN, KC channels per stage, and
-    // 3 (Gauss) or 4 real products per complex multiply-add
-    int con_bm, con_bn, con_kc, con_products;
+    // 3 (Gauss) or 4 real products per complex multiply-add; con_prefetch
+    // stages loaded ahead of the one being multiplied (1 to 3)
+    int con_bm, con_bn, con_kc, con_products, con_prefetch;
     // overlap-save band variant of the forward transform (band.hpp):
     // used if fwd_band; LDS row pitch, left zero columns, zero-row slot and
     // dynamic LDS bytes

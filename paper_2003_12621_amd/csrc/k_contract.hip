@@ -39,6 +39,31 @@ namespace fftsplit {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
+// s_waitcnt immediate that waits until at most n (< 64) vector memory
+// instructions are outstanding and leaves the other counters alone (gfx9
+// encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+constexpr int vmcnt_wait(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// 16 bytes per lane from global memory straight into LDS: lane l writes
+// LDS bytes [base + 16 l, base + 16 l + 16) with base the wave's LDS
+// address (the low 32 bits of a generic pointer into LDS are its LDS
+// offset).  Written as inline assembly rather than with the compiler's
+// builtin: for the builtin the compiler cannot tell which LDS buffer a load
+// fills and waits for all of them before every LDS read, which would
+// serialise the stages loaded ahead; here the caller waits (s_waitcnt
+// vmcnt) before the barrier that publishes a buffer.  One wait state
+// separates the M0 write from the load.
+template <bool NT>
+__device__ __forceinline__ void lds_dma16(const void* g, const void* lds_wave_base) {
+    const unsigned m0 = __builtin_amdgcn_readfirstlane(unsigned(reinterpret_cast<uintptr_t>(lds_wave_base)));
+    if constexpr (NT)
+        asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt" ::"v"(g), "s"(m0)
+                     : "memory", "m0");
+    else
+        asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m0)
+                     : "memory", "m0");
+}
+
 template <int BM, int BN, int KC, int WM>
 struct ConShape {
     static constexpr int NT = 256;
@@ -55,14 +80,13 @@ struct ConShape {
     static_assert((WE / 2) % NT == 0 && (XE / 2) % NT == 0, "loads divide evenly");
 };
 
-template <int BM, int BN, int KC, int WM, bool G3>
+template <int BM, int BN, int KC, int WM, bool G3, int PF>
 __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict__ xs, const float2* __restrict__ ws,
                                                        float2* __restrict__ ys, int cin, int coutp, int ntp,
                                                        int nbco, int nbt, int nbins, int ygroup, int npacked) {
     using S = ConShape<BM, BN, KC, WM>;
     constexpr int TM = S::TM, TN = S::TN;
-    extern __shared__ float4 lds_raw[];
-    float2* lds = reinterpret_cast<float2*>(lds_raw);   // [2][WE + XE]
+    extern __shared__ float4 lds_raw[];   // PF 1: two stage buffers
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -89,52 +113,55 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
         return reinterpret_cast<const float4*>(xs + spec_offset(ci, f, t0, nbins, ntp));
     };
 
-    uint4 wreg[S::WL], xreg[S::XL];
-    // A full stage is loaded as is; only a stage that runs past cin reads
-    // its missing rows from row cin-1 (always in range) and zeroes them.
-    // The branch is uniform, and in the full case the loaded registers are
-    // first used when the stage is written to LDS after the MFMAs, so the
-    // loads stay in flight during the multiply.
-    auto load_stage = [&](int k0) {
+    // register sets for the stages loaded ahead (the second only with PF 2)
+    typedef uint4 WRegs[S::WL];
+    typedef uint4 XRegs[S::XL];
+    WRegs wreg0, wreg1;
+    XRegs xreg0, xreg1;
+    // A stage that runs past cin reads its missing rows from row cin-1
+    // (always in range) and store_stage writes zeros for them.  The loads
+    // are never used before store_stage, so both kinds of stage leave them
+    // in flight through the multiply.
+    auto load_stage = [&](int k0, WRegs& wreg, XRegs& xreg) {
+        const bool full = k0 + KC <= cin;
+#pragma unroll
+        for (int i = 0; i < S::WL; ++i) {
+            const int e = i * S::NT + tid;
+            const int ci = k0 + e / (BM / 2);
+            wreg[i] = load_stream_u4(reinterpret_cast<const uint4*>(wsrc) + (full ? ci : min(ci, cin - 1)) * wrow4 +
+                                     e % (BM / 2));
+        }
+#pragma unroll
+        for (int i = 0; i < S::XL; ++i) {
+            const int e = i * S::NT + tid;
+            const int ci = k0 + e / (BN / 2);
+            xreg[i] = reinterpret_cast<const uint4*>(xrow(full ? ci : min(ci, cin - 1)))[e % (BN / 2)];
+        }
+    };
+    auto store_stage = [&](float2* stage, const WRegs& wreg, const XRegs& xreg, int k0) {
+        uint4* sw = reinterpret_cast<uint4*>(stage);
+        uint4* sx = reinterpret_cast<uint4*>(stage + S::WE);
+        auto masked = [](uint4 v, bool keep) {
+            const unsigned m = keep ? 0xffffffffu : 0u;
+            return make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
+        };
         if (k0 + KC <= cin) {
 #pragma unroll
-            for (int i = 0; i < S::WL; ++i) {
-                const int e = i * S::NT + tid;
-                wreg[i] = load_stream_u4(reinterpret_cast<const uint4*>(wsrc) + (k0 + e / (BM / 2)) * wrow4 +
-                                         e % (BM / 2));
-            }
+            for (int i = 0; i < S::WL; ++i) sw[i * S::NT + tid] = wreg[i];
 #pragma unroll
-            for (int i = 0; i < S::XL; ++i) {
-                const int e = i * S::NT + tid;
-                xreg[i] = reinterpret_cast<const uint4*>(xrow(k0 + e / (BN / 2)))[e % (BN / 2)];
-            }
+            for (int i = 0; i < S::XL; ++i) sx[i * S::NT + tid] = xreg[i];
         } else {
 #pragma unroll
             for (int i = 0; i < S::WL; ++i) {
                 const int e = i * S::NT + tid;
-                const int ci = k0 + e / (BM / 2);
-                const uint4 v = load_stream_u4(reinterpret_cast<const uint4*>(wsrc) + min(ci, cin - 1) * wrow4 +
-                                               e % (BM / 2));
-                const unsigned m = ci < cin ? 0xffffffffu : 0u;
-                wreg[i] = make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
+                sw[e] = masked(wreg[i], k0 + e / (BM / 2) < cin);
             }
 #pragma unroll
             for (int i = 0; i < S::XL; ++i) {
                 const int e = i * S::NT + tid;
-                const int ci = k0 + e / (BN / 2);
-                const uint4 v = reinterpret_cast<const uint4*>(xrow(min(ci, cin - 1)))[e % (BN / 2)];
-                const unsigned m = ci < cin ? 0xffffffffu : 0u;
-                xreg[i] = make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
+                sx[e] = masked(xreg[i], k0 + e / (BN / 2) < cin);
             }
         }
-    };
-    auto store_stage = [&](int buf) {
-        uint4* sw = reinterpret_cast<uint4*>(lds + buf * (S::WE + S::XE));
-        uint4* sx = reinterpret_cast<uint4*>(lds + buf * (S::WE + S::XE) + S::WE);
-#pragma unroll
-        for (int i = 0; i < S::WL; ++i) sw[i * S::NT + tid] = wreg[i];
-#pragma unroll
-        for (int i = 0; i < S::XL; ++i) sx[i * S::NT + tid] = xreg[i];
     };
 
     // 4M: accR = sum Wr Xr - Wi Xi, accI = sum Wr Xi + Wi Xr.
@@ -153,17 +180,12 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
             }
 
     const int nstage = (cin + KC - 1) / KC;
-    load_stage(0);
-    store_stage(0);
-    __syncthreads();
-
     const int krow = lane >> 5;
     const int col = lane & 31;
-    for (int s = 0; s < nstage; ++s) {
-        const int buf = s & 1;
-        if (s + 1 < nstage) load_stage((s + 1) * KC);
-        const float2* sw = lds + buf * (S::WE + S::XE) + krow * BM + wm * (TM * 32) + col;
-        const float2* sx = lds + buf * (S::WE + S::XE) + S::WE + krow * BN + wn * (TN * 32) + col;
+    // the multiply of the stage held in LDS buffer `buf`
+    auto multiply = [&](const float2* stage) {
+        const float2* sw = stage + krow * BM + wm * (TM * 32) + col;
+        const float2* sx = stage + S::WE + krow * BN + wn * (TN * 32) + col;
         float2 a[2][TM], b[2][TN];
 #pragma unroll
         for (int i = 0; i < TM; ++i) a[0][i] = sw[i * 32];
@@ -212,8 +234,86 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
                 }
             }
         }
-        if (s + 1 < nstage) store_stage(buf ^ 1);
+    };
+    if constexpr (PF == 1) {
+        float2* lds = reinterpret_cast<float2*>(lds_raw);   // [2][WE + XE]
+        load_stage(0, wreg0, xreg0);
+        store_stage(lds, wreg0, xreg0, 0);
         __syncthreads();
+        for (int s = 0; s < nstage; ++s) {
+            float2* cur = lds + (s & 1) * (S::WE + S::XE);
+            float2* nxt = lds + ((s + 1) & 1) * (S::WE + S::XE);
+            if (s + 1 < nstage) load_stage((s + 1) * KC, wreg0, xreg0);
+            multiply(cur);
+            if (s + 1 < nstage) store_stage(nxt, wreg0, xreg0, (s + 1) * KC);
+            __syncthreads();
+        }
+    } else {
+        // PF stages ahead, loaded straight into LDS (global_load_lds_dwordx4:
+        // lane l of a wave writes the 16 bytes at the wave's LDS base + 16 l,
+        // the layout store_stage writes), PF + 1 stage buffers.  The buffers
+        // are separate LDS variables and the loop is unrolled by PF + 1, so
+        // the register sets and LDS buffers are fixed at every step; the wait
+        // for a stage's own loads and the barrier are explicit
+        // (__syncthreads() would wait for every outstanding load, the stages
+        // ahead included).
+        constexpr int NB = PF + 1;
+        constexpr int SE = (S::WE + S::XE) / 2;   // float4 per stage buffer
+        __shared__ float4 ldsb0[SE], ldsb1[SE], ldsb2[SE], ldsb3[NB > 3 ? SE : 1];
+        float2* const bufs[4] = {reinterpret_cast<float2*>(ldsb0), reinterpret_cast<float2*>(ldsb1),
+                                 reinterpret_cast<float2*>(ldsb2), reinterpret_cast<float2*>(ldsb3)};
+        static_assert(NB <= 4, "at most four stage buffers");
+        constexpr int LPS = S::WL + S::XL;   // memory instructions per stage and thread
+        const int nfull = cin / KC;          // stages [0, nfull) are whole
+        auto dma_stage = [&](int k0, float2* stage) {
+            uint4* sw = reinterpret_cast<uint4*>(stage);
+            uint4* sx = reinterpret_cast<uint4*>(stage + S::WE);
+            const int wbase = tid & ~63;
+#pragma unroll
+            for (int i = 0; i < S::WL; ++i) {
+                const int e = i * S::NT + tid;
+                const uint4* g = reinterpret_cast<const uint4*>(wsrc) + (k0 + e / (BM / 2)) * wrow4 + e % (BM / 2);
+                lds_dma16<true>(g, sw + i * S::NT + wbase);   // non-temporal, as load_stream_u4
+            }
+#pragma unroll
+            for (int i = 0; i < S::XL; ++i) {
+                const int e = i * S::NT + tid;
+                const uint4* g = reinterpret_cast<const uint4*>(xrow(k0 + e / (BN / 2))) + e % (BN / 2);
+                lds_dma16<false>(g, sx + i * S::NT + wbase);
+            }
+        };
+        // full stage s in buffer `cur`; stage s + PF goes into `ahead` (the
+        // buffer of stage s - 1, which every wave has finished once past the
+        // barrier).  No register loads happen in this loop, so the compiler
+        // has no loads of its own to wait for.
+        auto step = [&](int s, float2* cur, float2* ahead) {
+            // this stage's loads are done when at most those of the stages
+            // issued after it remain (the memory counter retires in order)
+            const int later = min(s + PF - 1, nfull - 1) - s;
+            if (PF >= 3 && later >= 2) __builtin_amdgcn_s_waitcnt(vmcnt_wait(2 * LPS));
+            else if (later == 1) __builtin_amdgcn_s_waitcnt(vmcnt_wait(LPS));
+            else __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
+            asm volatile("s_barrier" ::: "memory");
+            if (s + PF < nfull) dma_stage((s + PF) * KC, ahead);
+            multiply(cur);
+        };
+#pragma unroll
+        for (int d = 0; d < PF; ++d)
+            if (d < nfull) dma_stage(d * KC, bufs[d]);
+        for (int s0 = 0; s0 < nfull; s0 += NB) {
+#pragma unroll
+            for (int r = 0; r < NB; ++r)
+                if (s0 + r < nfull) step(s0 + r, bufs[r], bufs[(r + PF) % NB]);
+        }
+        if (nfull < nstage) {
+            // the partial last stage, through registers (masked rows), once
+            // every wave is done with the buffers
+            __syncthreads();
+            load_stage(nfull * KC, wreg0, xreg0);
+            store_stage(bufs[0], wreg0, xreg0, nfull * KC);
+            __syncthreads();
+            multiply(bufs[0]);
+        }
     }
 
 #pragma unroll
@@ -243,17 +343,18 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     }
 }
 
-template <int BM, int BN, int KC, int WM, bool G3 = false>
+template <int BM, int BN, int KC, int WM, bool G3 = false, int PF = 1>
 static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, const float2* ws, float2* ys,
                                     hipStream_t s, const LaunchEvents& ev) {
     using S = ConShape<BM, BN, KC, WM>;
-    auto kern = contract_kernel<BM, BN, KC, WM, G3>;
-    static hipError_t attr = allow_dynamic_lds(kern, S::LDS_BYTES);
+    auto kern = contract_kernel<BM, BN, KC, WM, G3, PF>;
+    constexpr int lds = PF == 1 ? S::LDS_BYTES : 0;   // PF 2: static stage buffers
+    static hipError_t attr = allow_dynamic_lds(kern, lds);
     if (attr != hipSuccess) return attr;
     if (p.coutp % BM != 0 || p.ntp % BN != 0) return hipErrorInvalidValue;
     const int nbco = p.coutp / BM, nbt = p.ntp / BN;
     const size_t nb = size_t(nbco) * nbt * p.bins;
-    return launch_kernel(kern, dim3(unsigned(nb)), dim3(S::NT), S::LDS_BYTES, s, ev.start, ev.stop, xs, ws, ys,
+    return launch_kernel(kern, dim3(unsigned(nb)), dim3(S::NT), lds, s, ev.start, ev.stop, xs, ws, ys,
                          p.prob.cin, p.coutp, p.ntp, nbco, nbt, p.bins, patch_group(p.L), packed_slots(p.L));
 }
 
@@ -262,10 +363,15 @@ hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xs, const flo
     const int v = p.con_bm * 1000000 + p.con_bn * 1000 + p.con_kc;
     if (p.con_products == 3) {
         switch (v) {
-            case 64064016: return launch_contract_v<64, 64, 16, 2, true>(p, xs, ws, ys, s, ev);
+            case 64064016:
+                if (p.con_prefetch == 2) return launch_contract_v<64, 64, 16, 2, true, 2>(p, xs, ws, ys, s, ev);
+                if (p.con_prefetch == 3) return launch_contract_v<64, 64, 16, 2, true, 3>(p, xs, ws, ys, s, ev);
+                return launch_contract_v<64, 64, 16, 2, true>(p, xs, ws, ys, s, ev);
             case 128064016: return launch_contract_v<128, 64, 16, 2, true>(p, xs, ws, ys, s, ev);
             case 64128016: return launch_contract_v<64, 128, 16, 2, true>(p, xs, ws, ys, s, ev);
-            case 128032016: return launch_contract_v<128, 32, 16, 4, true>(p, xs, ws, ys, s, ev);
+            case 128032016:
+                if (p.con_prefetch == 2) return launch_contract_v<128, 32, 16, 4, true, 2>(p, xs, ws, ys, s, ev);
+                return launch_contract_v<128, 32, 16, 4, true>(p, xs, ws, ys, s, ev);
         }
     } else {
         switch (v) {

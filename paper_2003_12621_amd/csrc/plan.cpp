@@ -288,6 +288,12 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     plan->con_bn = g.ntp % 64 == 0 ? 64 : 32;
     plan->con_kc = 16;
     plan->con_products = 3;
+    // two stages ahead, through LDS (the tiles that have that variant)
+    plan->con_prefetch = 2;
+    if (const char* v = std::getenv("FFTSPLIT_CONTRACT_PREFETCH")) {
+        const int pf = std::atoi(v);
+        if (pf >= 1 && pf <= 3) plan->con_prefetch = pf;
+    }
     if (const char* v = std::getenv("FFTSPLIT_CONTRACT_TILE")) {
         if (*v) {
             int prod = 4;
@@ -304,6 +310,15 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
             plan->con_kc = kc;
             plan->con_products = prod;
         }
+    }
+    // the LDS-prefetch variants exist for the 3-product 64x64x16 and
+    // 128x32x16 tiles (and three stages ahead for 64x64x16 only)
+    {
+        const bool lds_variant = plan->con_products == 3 && plan->con_kc == 16 &&
+                                 ((plan->con_bm == 64 && plan->con_bn == 64) ||
+                                  (plan->con_bm == 128 && plan->con_bn == 32));
+        if (!lds_variant) plan->con_prefetch = 1;
+        if (plan->con_prefetch == 3 && plan->con_bm != 64) plan->con_prefetch = 2;
     }
     if (g.coutp % plan->con_bm != 0 || g.ntp % plan->con_bn != 0) {
         const int bm = plan->con_bm, bn = plan->con_bn;
@@ -390,6 +405,7 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_plan_info(fftsplit_plan_t plan, fftsp
     i.direct_wspec_bytes = direct_wspec_bytes(*plan);
     i.spec_group = patch_group(plan->L);
     i.fused_channel_sum = plan->fuse_cin ? 1 : 0;
+    i.contract_prefetch = plan->con_prefetch;
     *out = i;
     return FFTSPLIT_SUCCESS;
 }

@@ -259,3 +259,23 @@ def test_size_limits():
     assert status_of(n=700, cin=256, h=56, w=56, cout=16, k=5, tile=28) == fs.ERROR_NOT_SUPPORTED
     # image plane above 2^31 pixels
     assert status_of(n=1, cin=1, h=50000, w=50000, cout=1, k=3, tile=6) == fs.ERROR_NOT_SUPPORTED
+
+
+def test_contraction_prefetch_choice(monkeypatch):
+    """The 3-product 64x64x16 and 128x32x16 tiles load two input-channel
+    stages ahead through LDS; other tiles one, through registers; the
+    environment variable overrides within what the tile has."""
+    monkeypatch.delenv("FFTSPLIT_CONTRACT_PREFETCH", raising=False)
+    monkeypatch.delenv("FFTSPLIT_CONTRACT_TILE", raising=False)
+    assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.contract_prefetch == 2
+    assert plan(n=32, cin=512, h=14, w=14, cout=512, k=3, tile=14).info.contract_prefetch == 2   # 128 x 32
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", "g4:64x64x16")
+    assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.contract_prefetch == 1
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", "g3:128x64x16")
+    assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.contract_prefetch == 1
+    monkeypatch.delenv("FFTSPLIT_CONTRACT_TILE")
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_PREFETCH", "1")
+    assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.contract_prefetch == 1
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_PREFETCH", "3")
+    assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.contract_prefetch == 3
+    assert plan(n=32, cin=512, h=14, w=14, cout=512, k=3, tile=14).info.contract_prefetch == 2

@@ -151,3 +151,39 @@ def test_maxpool_exact():
         x = rng.standard_normal(shape).astype(np.float32)
         got = fs.maxpool2x2(_dev(x)).cpu().numpy()
         np.testing.assert_array_equal(got, oracle.maxpool2x2(x))
+
+
+@pytest.mark.parametrize("prefetch", ["1", "2", "3"])
+@pytest.mark.parametrize("cin", [16, 32, 40, 48, 64, 80, 100])
+@pytest.mark.parametrize("cout", [64, 128])
+def test_contraction_stage_pipeline(cin, cout, prefetch, monkeypatch):
+    """The contraction's input-channel pipeline (stages of 16 channels loaded
+    one, two or three stages ahead; a partial last stage; 64 x 64 tiles, and
+    128 x 32 where 32 patches are padded) against the oracle's channel sum,
+    and bit-identical across prefetch depths (same products, same order)."""
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_PREFETCH", prefetch)
+    shape = (2, cin, 24, 24, cout, 3)
+    x, wt = small_layer(*shape, seed=cin)
+    plan = fs.Plan(*shape, tile=14)
+    print(f"[case] cin={cin} cout={cout} prefetch={plan.info.contract_prefetch} "
+          f"tile={plan.info.contract_tile_m}x{plan.info.contract_tile_n}", flush=True)
+    ws = plan.new_workspace()
+    wspec = plan.transform_weights(_dev(wt))
+    plan.forward(_dev(x), ws)
+    plan.contract(wspec, ws)
+    torch.cuda.synchronize()
+    X = plan.xspec_view(ws).cpu().numpy().astype(np.complex128)
+    W = plan.wspec_view(wspec).cpu().numpy().astype(np.complex128)
+    Y = plan.yspec_view(ws).cpu().numpy()
+    ref = oracle.hadamard_channel_sum(X.transpose(2, 1, 0), np.conj(W).transpose(2, 1, 0)).transpose(2, 1, 0)
+    for f in (-2, -1):
+        ref[f] = (np.einsum("ic,it->ct", W[f].real, X[f].real)
+                  + 1j * np.einsum("ic,it->ct", W[f].imag, X[f].imag))
+    assert rel_l2(Y, ref) < 2e-6
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_PREFETCH", "1")
+    plan1 = fs.Plan(*shape, tile=14)
+    ws1 = plan1.new_workspace()
+    plan1.forward(_dev(x), ws1)
+    plan1.contract(plan1.transform_weights(_dev(wt)), ws1)
+    torch.cuda.synchronize()
+    assert np.array_equal(plan1.yspec_view(ws1).cpu().numpy(), Y)
