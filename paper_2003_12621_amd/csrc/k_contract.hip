@@ -200,6 +200,9 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
 #pragma unroll
                 for (int j = 0; j < TN; ++j) b[cur ^ 1][j] = sx[(2 * kp + 2) * BN + j * 32];
             }
+            // the next channel pair's fragment reads stay ahead of this
+            // pair's matrix products
+            __builtin_amdgcn_sched_barrier(0);
             if (G3) {
                 float bs_[TN];
 #pragma unroll
