@@ -86,7 +86,7 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
                                                        int nbco, int nbt, int nbins, int ygroup, int npacked) {
     using S = ConShape<BM, BN, KC, WM>;
     constexpr int TM = S::TM, TN = S::TN;
-    extern __shared__ float4 lds_raw[];   // PF 1: two stage buffers
+    extern __shared__ float4 lds_raw[];   // max(PF + 1, 2) stage buffers
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -254,17 +254,14 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     } else {
         // PF stages ahead, loaded straight into LDS (global_load_lds_dwordx4:
         // lane l of a wave writes the 16 bytes at the wave's LDS base + 16 l,
-        // the layout store_stage writes), PF + 1 stage buffers.  The buffers
-        // are separate LDS variables and the loop is unrolled by PF + 1, so
-        // the register sets and LDS buffers are fixed at every step; the wait
-        // for a stage's own loads and the barrier are explicit
-        // (__syncthreads() would wait for every outstanding load, the stages
-        // ahead included).
+        // the layout store_stage writes), PF + 1 stage buffers in the dynamic
+        // LDS.  The loop is unrolled by PF + 1, so the buffers are fixed at
+        // every step; the wait for a stage's own loads and the barrier are
+        // explicit (__syncthreads() would wait for every outstanding load,
+        // the stages ahead included).
         constexpr int NB = PF + 1;
-        constexpr int SE = (S::WE + S::XE) / 2;   // float4 per stage buffer
-        __shared__ float4 ldsb0[SE], ldsb1[SE], ldsb2[SE], ldsb3[NB > 3 ? SE : 1];
-        float2* const bufs[4] = {reinterpret_cast<float2*>(ldsb0), reinterpret_cast<float2*>(ldsb1),
-                                 reinterpret_cast<float2*>(ldsb2), reinterpret_cast<float2*>(ldsb3)};
+        float2* const lds = reinterpret_cast<float2*>(lds_raw);
+        float2* const bufs[4] = {lds, lds + (S::WE + S::XE), lds + 2 * (S::WE + S::XE), lds + 3 * (S::WE + S::XE)};
         static_assert(NB <= 4, "at most four stage buffers");
         constexpr int LPS = S::WL + S::XL;   // memory instructions per stage and thread
         const int nfull = cin / KC;          // stages [0, nfull) are whole
@@ -351,7 +348,7 @@ static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, 
                                     hipStream_t s, const LaunchEvents& ev) {
     using S = ConShape<BM, BN, KC, WM>;
     auto kern = contract_kernel<BM, BN, KC, WM, G3, PF>;
-    constexpr int lds = PF == 1 ? S::LDS_BYTES : 0;   // PF 2: static stage buffers
+    constexpr int lds = (PF > 1 ? PF + 1 : 2) * (S::WE + S::XE) * 8;
     static hipError_t attr = allow_dynamic_lds(kern, lds);
     if (attr != hipSuccess) return attr;
     if (p.coutp % BM != 0 || p.ntp % BN != 0) return hipErrorInvalidValue;
@@ -370,8 +367,12 @@ hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xs, const flo
                 if (p.con_prefetch == 2) return launch_contract_v<64, 64, 16, 2, true, 2>(p, xs, ws, ys, s, ev);
                 if (p.con_prefetch == 3) return launch_contract_v<64, 64, 16, 2, true, 3>(p, xs, ws, ys, s, ev);
                 return launch_contract_v<64, 64, 16, 2, true>(p, xs, ws, ys, s, ev);
-            case 128064016: return launch_contract_v<128, 64, 16, 2, true>(p, xs, ws, ys, s, ev);
-            case 64128016: return launch_contract_v<64, 128, 16, 2, true>(p, xs, ws, ys, s, ev);
+            case 128064016:
+                if (p.con_prefetch == 2) return launch_contract_v<128, 64, 16, 2, true, 2>(p, xs, ws, ys, s, ev);
+                return launch_contract_v<128, 64, 16, 2, true>(p, xs, ws, ys, s, ev);
+            case 64128016:
+                if (p.con_prefetch == 2) return launch_contract_v<64, 128, 16, 2, true, 2>(p, xs, ws, ys, s, ev);
+                return launch_contract_v<64, 128, 16, 2, true>(p, xs, ws, ys, s, ev);
             case 128032016:
                 if (p.con_prefetch == 2) return launch_contract_v<128, 32, 16, 4, true, 2>(p, xs, ws, ys, s, ev);
                 return launch_contract_v<128, 32, 16, 4, true>(p, xs, ws, ys, s, ev);

@@ -311,12 +311,15 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
             plan->con_products = prod;
         }
     }
-    // the LDS-prefetch variants exist for the 3-product 64x64x16 and
-    // 128x32x16 tiles (and three stages ahead for 64x64x16 only)
+    // the LDS-prefetch variants exist for the 3-product 64x64, 128x32,
+    // 128x64 and 64x128 tiles with 16-channel stages (three stages ahead
+    // for 64x64 only)
     {
         const bool lds_variant = plan->con_products == 3 && plan->con_kc == 16 &&
                                  ((plan->con_bm == 64 && plan->con_bn == 64) ||
-                                  (plan->con_bm == 128 && plan->con_bn == 32));
+                                  (plan->con_bm == 128 && plan->con_bn == 32) ||
+                                  (plan->con_bm == 128 && plan->con_bn == 64) ||
+                                  (plan->con_bm == 64 && plan->con_bn == 128));
         if (!lds_variant) plan->con_prefetch = 1;
         if (plan->con_prefetch == 3 && plan->con_bm != 64) plan->con_prefetch = 2;
     }

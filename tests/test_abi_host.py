@@ -262,9 +262,10 @@ def test_size_limits():
 
 
 def test_contraction_prefetch_choice(monkeypatch):
-    """The 3-product 64x64x16 and 128x32x16 tiles load two input-channel
-    stages ahead through LDS; other tiles one, through registers; the
-    environment variable overrides within what the tile has."""
+    """The 3-product tiles with 16-channel stages (64x64, 128x32, 128x64,
+    64x128) load two input-channel stages ahead through LDS; other tiles
+    one, through registers; the environment variable overrides within what
+    the tile has."""
     monkeypatch.delenv("FFTSPLIT_CONTRACT_PREFETCH", raising=False)
     monkeypatch.delenv("FFTSPLIT_CONTRACT_TILE", raising=False)
     assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.contract_prefetch == 2
@@ -272,6 +273,8 @@ def test_contraction_prefetch_choice(monkeypatch):
     monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", "g4:64x64x16")
     assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.contract_prefetch == 1
     monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", "g3:128x64x16")
+    assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.contract_prefetch == 2
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", "g3:64x64x32")
     assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.contract_prefetch == 1
     monkeypatch.delenv("FFTSPLIT_CONTRACT_TILE")
     monkeypatch.setenv("FFTSPLIT_CONTRACT_PREFETCH", "1")

@@ -187,3 +187,31 @@ def test_contraction_stage_pipeline(cin, cout, prefetch, monkeypatch):
     plan1.contract(plan1.transform_weights(_dev(wt)), ws1)
     torch.cuda.synchronize()
     assert np.array_equal(plan1.yspec_view(ws1).cpu().numpy(), Y)
+
+
+@pytest.mark.parametrize("tile_env,n", [("g3:128x64x16", 16), ("g3:64x128x16", 32)])
+def test_contraction_other_tiles(tile_env, n, monkeypatch):
+    """The 128 x 64 and 64 x 128 tiles (plan options), both prefetch depths,
+    against the oracle's channel sum and bit-identical to each other."""
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", tile_env)
+    shape = (n, 40, 24, 24, 128, 3)
+    x, wt = small_layer(*shape, seed=11)
+    outs = []
+    for pf in ("1", "2"):
+        monkeypatch.setenv("FFTSPLIT_CONTRACT_PREFETCH", pf)
+        plan = fs.Plan(*shape, tile=14)
+        print(f"[case] {tile_env} n={n} prefetch={plan.info.contract_prefetch}", flush=True)
+        ws = plan.new_workspace()
+        wspec = plan.transform_weights(_dev(wt))
+        plan.forward(_dev(x), ws)
+        plan.contract(wspec, ws)
+        torch.cuda.synchronize()
+        outs.append(plan.yspec_view(ws).cpu().numpy())
+    X = plan.xspec_view(ws).cpu().numpy().astype(np.complex128)
+    W = plan.wspec_view(wspec).cpu().numpy().astype(np.complex128)
+    ref = oracle.hadamard_channel_sum(X.transpose(2, 1, 0), np.conj(W).transpose(2, 1, 0)).transpose(2, 1, 0)
+    for f in (-2, -1):
+        ref[f] = (np.einsum("ic,it->ct", W[f].real, X[f].real)
+                  + 1j * np.einsum("ic,it->ct", W[f].imag, X[f].imag))
+    assert rel_l2(outs[1], ref) < 2e-6
+    assert np.array_equal(outs[0], outs[1])
