@@ -80,6 +80,41 @@ struct ConShape {
     static_assert((WE / 2) % NT == 0 && (XE / 2) % NT == 0, "loads divide evenly");
 };
 
+// Writes a wave's TM x TN MFMA tiles of output spectra (rows from co_base,
+// patches from t_base) in the patch-group-major layout: the 32 lanes of a
+// row write 32 consecutive patches (32 / G runs of G, or half a run).
+// With G3, Y = (P1 - P2, P3 - P1 - P2), except in the two slots of packed
+// real bins, whose parts are P1 and P2 themselves.
+template <int TM, int TN, bool G3>
+__device__ __forceinline__ void store_output_tile(float2* __restrict__ ys, const floatx16 (&accR)[TM][TN],
+                                                  const floatx16 (&accI)[TM][TN],
+                                                  const floatx16 (&acc3)[G3 ? TM : 1][G3 ? TN : 1], int co_base,
+                                                  int t_base, int f, int nbins, int ygroup, int ntp, int krow,
+                                                  int col, bool packed) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int cb0 = co_base + i * 32;
+            float2* yb = ys + yspec_offset(cb0, f, t_base + j * 32 + col, nbins, ygroup, ntp / ygroup);
+            const size_t cstride = size_t(nbins) * ntp;   // next channel
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                // row ii = 8 (r / 4) + 4 krow + r % 4 of the 32
+                const int ii = 8 * (r >> 2) + 4 * krow + (r & 3);
+                float2* dst = yb + size_t(ii) * cstride;
+                if (G3) {
+                    const float p1 = accR[i][j][r], p2 = accI[i][j][r];
+                    *dst = packed ? make_float2(p1, p2)
+                                  : make_float2(p1 - p2, acc3[G3 ? i : 0][G3 ? j : 0][r] - p1 - p2);
+                } else {
+                    *dst = make_float2(accR[i][j][r], accI[i][j][r]);
+                }
+            }
+        }
+    }
+}
+
 template <int BM, int BN, int KC, int WM, bool G3, int PF>
 __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict__ xs, const float2* __restrict__ ws,
                                                        float2* __restrict__ ys, int cin, int coutp, int ntp,
@@ -316,31 +351,8 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
         }
     }
 
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            // output spectra, patch-group-major: the 32 lanes of a row write
-            // 32 consecutive patches (32 / G runs of G, or half a run)
-            const int cb0 = co0 + wm * (TM * 32) + i * 32;
-            float2* yb = ys + yspec_offset(cb0, f, t0 + wn * (TN * 32) + j * 32 + col, nbins, ygroup,
-                                           ntp / ygroup);
-            const size_t cstride = size_t(nbins) * ntp;   // next channel
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                // row ii = 8 (r / 4) + 4 krow + r % 4 of the 32
-                const int ii = 8 * (r >> 2) + 4 * krow + (r & 3);
-                float2* dst = yb + size_t(ii) * cstride;
-                if (G3) {
-                    const float p1 = accR[i][j][r], p2 = accI[i][j][r];
-                    *dst = packed ? make_float2(p1, p2)
-                                  : make_float2(p1 - p2, acc3[G3 ? i : 0][G3 ? j : 0][r] - p1 - p2);
-                } else {
-                    *dst = make_float2(accR[i][j][r], accI[i][j][r]);
-                }
-            }
-        }
-    }
+    store_output_tile<TM, TN, G3>(ys, accR, accI, acc3, co0 + wm * (TM * 32), t0 + wn * (TN * 32), f, nbins, ygroup,
+                                  ntp, krow, col, packed);
 }
 
 template <int BM, int BN, int KC, int WM, bool G3 = false, int PF = 1>
