@@ -115,6 +115,70 @@ __device__ __forceinline__ void store_output_tile(float2* __restrict__ ys, const
     }
 }
 
+// One input-channel stage (KC channels) of a wave's TM x TN MFMA tiles,
+// from the stage buffer in LDS (W rows of BM channels, then X rows of BN
+// patches).  The fragments of the next channel pair are read while the
+// current pair is multiplied.
+template <int BM, int BN, int KC, int TM, int TN, bool G3>
+__device__ __forceinline__ void multiply_stage(const float2* stage, floatx16 (&accR)[TM][TN],
+                                               floatx16 (&accI)[TM][TN],
+                                               floatx16 (&acc3)[G3 ? TM : 1][G3 ? TN : 1], int krow, int col,
+                                               int wm, int wn, bool packed) {
+    const float2* sw = stage + krow * BM + wm * (TM * 32) + col;
+    const float2* sx = stage + KC * BM + krow * BN + wn * (TN * 32) + col;
+    float2 a[2][TM], b[2][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) a[0][i] = sw[i * 32];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) b[0][j] = sx[j * 32];
+#pragma unroll
+    for (int kp = 0; kp < KC / 2; ++kp) {
+        const int cur = kp & 1;
+        if (kp + 1 < KC / 2) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) a[cur ^ 1][i] = sw[(2 * kp + 2) * BM + i * 32];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) b[cur ^ 1][j] = sx[(2 * kp + 2) * BN + j * 32];
+        }
+        // the next channel pair's fragment reads stay ahead of this
+        // pair's matrix products
+        __builtin_amdgcn_sched_barrier(0);
+        if (G3) {
+            float bs_[TN];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) bs_[j] = b[cur][j].x + b[cur][j].y;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const float ar = a[cur][i].x, ai = a[cur][i].y, as_ = ar + ai;
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ar, b[cur][j].x, accR[i][j], 0, 0, 0);
+                    accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ai, b[cur][j].y, accI[i][j], 0, 0, 0);
+                    acc3[G3 ? i : 0][G3 ? j : 0] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                        as_, bs_[j], acc3[G3 ? i : 0][G3 ? j : 0], 0, 0, 0);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                // a slot of two real bins: accR = sum Wr Xr, accI = sum Wi Xi
+                const float ar = a[cur][i].x, ai = a[cur][i].y;
+                const float a2 = packed ? ai : ar, nai = packed ? 0.f : -ai, ai4 = packed ? 0.f : ai;
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ar, b[cur][j].x, accR[i][j], 0, 0, 0);
+                    accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a2, b[cur][j].y, accI[i][j], 0, 0, 0);
+                }
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(nai, b[cur][j].y, accR[i][j], 0, 0, 0);
+                    accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ai4, b[cur][j].x, accI[i][j], 0, 0, 0);
+                }
+            }
+        }
+    }
+}
+
 template <int BM, int BN, int KC, int WM, bool G3, int PF>
 __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict__ xs, const float2* __restrict__ ws,
                                                        float2* __restrict__ ys, int cin, int coutp, int ntp,
@@ -217,61 +281,9 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     const int nstage = (cin + KC - 1) / KC;
     const int krow = lane >> 5;
     const int col = lane & 31;
-    // the multiply of the stage held in LDS buffer `buf`
+    // the multiply of the stage held in LDS buffer `stage`
     auto multiply = [&](const float2* stage) {
-        const float2* sw = stage + krow * BM + wm * (TM * 32) + col;
-        const float2* sx = stage + S::WE + krow * BN + wn * (TN * 32) + col;
-        float2 a[2][TM], b[2][TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i) a[0][i] = sw[i * 32];
-#pragma unroll
-        for (int j = 0; j < TN; ++j) b[0][j] = sx[j * 32];
-#pragma unroll
-        for (int kp = 0; kp < KC / 2; ++kp) {
-            const int cur = kp & 1;
-            if (kp + 1 < KC / 2) {
-#pragma unroll
-                for (int i = 0; i < TM; ++i) a[cur ^ 1][i] = sw[(2 * kp + 2) * BM + i * 32];
-#pragma unroll
-                for (int j = 0; j < TN; ++j) b[cur ^ 1][j] = sx[(2 * kp + 2) * BN + j * 32];
-            }
-            // the next channel pair's fragment reads stay ahead of this
-            // pair's matrix products
-            __builtin_amdgcn_sched_barrier(0);
-            if (G3) {
-                float bs_[TN];
-#pragma unroll
-                for (int j = 0; j < TN; ++j) bs_[j] = b[cur][j].x + b[cur][j].y;
-#pragma unroll
-                for (int i = 0; i < TM; ++i) {
-                    const float ar = a[cur][i].x, ai = a[cur][i].y, as_ = ar + ai;
-#pragma unroll
-                    for (int j = 0; j < TN; ++j) {
-                        accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ar, b[cur][j].x, accR[i][j], 0, 0, 0);
-                        accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ai, b[cur][j].y, accI[i][j], 0, 0, 0);
-                        acc3[G3 ? i : 0][G3 ? j : 0] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                            as_, bs_[j], acc3[G3 ? i : 0][G3 ? j : 0], 0, 0, 0);
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int i = 0; i < TM; ++i) {
-                    // a slot of two real bins: accR = sum Wr Xr, accI = sum Wi Xi
-                    const float ar = a[cur][i].x, ai = a[cur][i].y;
-                    const float a2 = packed ? ai : ar, nai = packed ? 0.f : -ai, ai4 = packed ? 0.f : ai;
-#pragma unroll
-                    for (int j = 0; j < TN; ++j) {
-                        accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ar, b[cur][j].x, accR[i][j], 0, 0, 0);
-                        accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a2, b[cur][j].y, accI[i][j], 0, 0, 0);
-                    }
-#pragma unroll
-                    for (int j = 0; j < TN; ++j) {
-                        accR[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(nai, b[cur][j].y, accR[i][j], 0, 0, 0);
-                        accI[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(ai4, b[cur][j].x, accI[i][j], 0, 0, 0);
-                    }
-                }
-            }
-        }
+        multiply_stage<BM, BN, KC, TM, TN, G3>(stage, accR, accI, acc3, krow, col, wm, wn, packed);
     };
     if constexpr (PF == 1) {
         float2* lds = reinterpret_cast<float2*>(lds_raw);   // [2][WE + XE]
