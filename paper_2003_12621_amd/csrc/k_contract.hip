@@ -23,15 +23,17 @@
 // operand fragment; the plan's default.
 //
 // Workgroup tile: BM output channels x BN patches of one bin, 4 waves in a
-// WM x (4/WM) grid.  The input-channel loop runs in stages of KC channels;
+// WM x (4/WM) grid.  The input-channel loop runs in stages of KC channels.
+// PF = 2 (the default where a tile has it): stages are loaded two ahead
+// straight into three LDS stage buffers, one barrier per stage.  PF = 1:
 // stage s+1 is loaded from memory into registers while stage s is
-// multiplied out of LDS, then written to the other LDS buffer (one barrier
-// per stage).  Inside a stage the operand fragments of the next channel
-// pair are read from LDS while the current pair's MFMAs run.  The filter
-// spectra, the bulk of the bytes and each read once, are loaded
-// non-temporally so they do not evict the patch and output spectra.  The channel
-// blocks of one bin are consecutive logical workgroups on the same XCD, so
-// the bin's patch spectra are fetched from HBM once and reused from L2.
+// multiplied out of LDS, then written to the other LDS buffer.  Inside a
+// stage the operand fragments of the next channel pair are read from LDS
+// while the current pair's MFMAs run.  The filter spectra, the bulk of the
+// bytes and each read once, are loaded non-temporally so they do not evict
+// the patch and output spectra.  The channel blocks of one bin are
+// consecutive logical workgroups on the same XCD, so the bin's patch
+// spectra are fetched from HBM once and reused from L2.
 #include "fftsplit_internal.hpp"
 #include "launch_util.hpp"
 
