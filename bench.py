@@ -264,7 +264,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for {args.gpus}); the multi-GPU "
+        print(f"bench.py: the library runs on one GPU only (asked for {args.gpus}); the multi-GPU "
               "sharding of the path is a design note, not an implementation.", file=sys.stderr)
         sys.exit(2)
 
