@@ -221,38 +221,76 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
 // either direction) sums the aux entries of the 1-4 patches covering it, in
 // the order (a0-1, b0-1), (a0-1, b0), (a0, b0-1), (a0, b0), then adds the
 // bias and applies ReLU.  Core pixels were written by inverse_kernel.
+// Seam pixels of a plane are enumerated compactly: indices below nsr * w
+// walk the seam rows (all columns), the rest walk the seam columns of the
+// other rows.  Seam rows are those with (r + P) mod T < 2P; the k-th is
+// ((k + P) / 2P) T - P + (k + P) mod 2P (likewise for columns); the k-th
+// other row is (k / (T - 2P)) T + P + k mod (T - 2P).  A thread takes
+// kSeamPix pixels and issues all their loads before any sum: a missing
+// contribution reads an out-of-range offset of a descriptor over the
+// plane's patch results, which returns 0, so every pixel sums four terms in
+// the fixed order (adding +0 leaves a sum unchanged).
+constexpr int kSeamPix = 4;
+
 __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux, const float* __restrict__ bias,
                                                    float* __restrict__ y, int cout, int h, int w, int T, int P, int L,
-                                                   int th, int tw, int ntp, int relu) {
+                                                   int th, int tw, int ntp, int relu, int nsr, int nsc) {
     const int plane = blockIdx.y;
-    const int idx = blockIdx.x * 256 + threadIdx.x;
-    if (idx >= h * w) return;
-    const int r = idx / w, c = idx % w;
-    const bool seam_r = (r + P) % T < 2 * P;
-    const bool seam_c = (c + P) % T < 2 * P;
-    if (!seam_r && !seam_c) return;
     const int img = plane / cout, co = plane % cout;
-    const int a0 = (r + P) / T, b0 = (c + P) / T;
-    float acc = 0.f;
+    const int P2 = 2 * P, LL = L * L;
+    const BufRsrc rin = make_rsrc(aux + (size_t(co) * ntp + size_t(img) * th * tw) * LL, unsigned(th * tw * LL * 4));
+    const int n_row = nsr * w, n_all = n_row + (h - nsr) * nsc;
+    float v[kSeamPix][4];
+    int out[kSeamPix];
 #pragma unroll
-    for (int da = 1; da >= 0; --da) {
-        const int a = a0 - da;
-        if ((da && !seam_r) || a < 0 || a >= th) continue;
-        int p = r - a * T - P;
-        if (p < 0) p += L;
+    for (int i = 0; i < kSeamPix; ++i) {
+        const int idx = (blockIdx.x * kSeamPix + i) * 256 + threadIdx.x;
+        int r = 0, c = 0;
+        bool seam_r = true;
+        if (idx < n_row) {
+            const int k = idx / w;
+            c = idx - k * w;
+            r = ((k + P) / P2) * T - P + (k + P) % P2;
+        } else if (idx < n_all) {
+            const int j = idx - n_row;
+            const int k = j / nsc, sc = j - k * nsc;
+            const int cs = T - P2;
+            r = (k / cs) * T + P + k % cs;
+            c = ((sc + P) / P2) * T - P + (sc + P) % P2;
+            seam_r = false;
+        }
+        const bool live = idx < n_all;
+        out[i] = live ? r * w + c : -1;
+        const bool seam_c = (c + P) % T < P2;
+        const int a0 = (r + P) / T, b0 = (c + P) / T;
 #pragma unroll
-        for (int db = 1; db >= 0; --db) {
-            const int b = b0 - db;
-            if ((db && !seam_c) || b < 0 || b >= tw) continue;
-            int qq = c - b * T - P;
-            if (qq < 0) qq += L;
-            const int t = (img * th + a) * tw + b;
-            acc += aux[((co * ntp + t) * L + p) * L + qq];
+        for (int da = 1; da >= 0; --da) {
+            const int a = a0 - da;
+            int p = r - a * T - P;
+            if (p < 0) p += L;
+            const bool ok_a = live && (!da || seam_r) && a >= 0 && a < th;
+#pragma unroll
+            for (int db = 1; db >= 0; --db) {
+                const int b = b0 - db;
+                int qq = c - b * T - P;
+                if (qq < 0) qq += L;
+                const bool ok = ok_a && (!db || seam_c) && b >= 0 && b < tw;
+                const unsigned off = ok ? unsigned(((a * tw + b) * L + p) * L + qq) * 4u : kOutOfRange;
+                v[i][2 * (1 - da) + (1 - db)] = buf_load_f32(rin, off, 0);
+            }
         }
     }
-    float v = acc + (bias ? bias[co] : 0.f);
-    if (relu) v = fmaxf(v, 0.f);
-    y[(size_t(plane) * h + r) * w + c] = v;
+    const float bv = bias ? bias[co] : 0.f;
+    float* yp = y + size_t(plane) * h * w;
+#pragma unroll
+    for (int i = 0; i < kSeamPix; ++i) {
+        float acc = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc += v[i][j];
+        float o = acc + bv;
+        if (relu) o = fmaxf(o, 0.f);
+        if (out[i] >= 0) yp[out[i]] = o;
+    }
 }
 
 
@@ -839,9 +877,17 @@ static hipError_t launch_inverse_v(const fftsplit_plan_s& p, const float2* ys, c
 
 hipError_t launch_seam(const fftsplit_plan_s& p, const float* aux, const float* bias, float* y, hipStream_t s,
                        hipEvent_t stop) {
-    const dim3 sgrid(unsigned((p.prob.h * p.prob.w + 255) / 256), unsigned(p.prob.n * p.prob.cout));
+    // seam rows (columns): r in [0, h) with (r + P) mod T < 2P, counted as
+    // u = r + P over [P, h + P) with u mod T < 2P
+    const int T = p.T, P2 = 2 * p.P;
+    auto below = [&](int n) { return (n / T) * (P2 < T ? P2 : T) + (n % T < P2 ? n % T : P2); };
+    const int nsr = below(p.prob.h + p.P) - below(p.P);
+    const int nsc = below(p.prob.w + p.P) - below(p.P);
+    const long long count = (long long)nsr * p.prob.w + (long long)(p.prob.h - nsr) * nsc;
+    const long long per_block = 256LL * kSeamPix;
+    const dim3 sgrid(unsigned(count > 0 ? (count + per_block - 1) / per_block : 1), unsigned(p.prob.n * p.prob.cout));
     return launch_kernel(seam_kernel, sgrid, dim3(256), 0, s, nullptr, stop, aux, bias, y, p.prob.cout, p.prob.h,
-                         p.prob.w, p.T, p.P, p.L, p.th, p.tw, p.ntp, int(p.relu));
+                         p.prob.w, p.T, p.P, p.L, p.th, p.tw, p.ntp, int(p.relu), nsr, nsc);
 }
 
 template <int L, int TG>

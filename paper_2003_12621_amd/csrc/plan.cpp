@@ -212,6 +212,9 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     // The overlap-add seam buffer is indexed with 32-bit offsets.
     if (oaa && size_t(p.cout) * size_t(g.ntp) * size_t(g.L) * size_t(g.L) > size_t(INT_MAX))
         return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "overlap-add seam buffer above 2^31 elements is not supported");
+    // The seam pass addresses one image plane's patch results in bytes below 2^31.
+    if (oaa && size_t(g.th) * size_t(g.tw) * size_t(g.L) * size_t(g.L) >= (size_t(1) << 29))
+        return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "overlap-add results of one image above 2^29 elements are not supported");
     // The contraction indexes one bin's spectra with 32-bit offsets.
     if (size_t(p.cin) * size_t(g.coutp) > size_t(INT_MAX) || size_t(p.cin) * size_t(g.ntp) > size_t(INT_MAX) ||
         size_t(g.coutp) * size_t(g.ntp) > size_t(INT_MAX))
