@@ -234,8 +234,10 @@ constexpr int kSeamPix = 4;
 
 __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux, const float* __restrict__ bias,
                                                    float* __restrict__ y, int cout, int h, int w, int T, int P, int L,
-                                                   int th, int tw, int ntp, int relu, int nsr, int nsc) {
-    const int plane = blockIdx.y;
+                                                   int th, int tw, int ntp, int relu, int nsr, int nsc, int bpp) {
+    // blocks run plane-major, bpp blocks per plane
+    const int plane = blockIdx.x / bpp;
+    const int blk = blockIdx.x - plane * bpp;
     const int img = plane / cout, co = plane % cout;
     const int P2 = 2 * P, LL = L * L;
     const BufRsrc rin = make_rsrc(aux + (size_t(co) * ntp + size_t(img) * th * tw) * LL, unsigned(th * tw * LL * 4));
@@ -244,7 +246,7 @@ __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux
     int out[kSeamPix];
 #pragma unroll
     for (int i = 0; i < kSeamPix; ++i) {
-        const int idx = (blockIdx.x * kSeamPix + i) * 256 + threadIdx.x;
+        const int idx = (blk * kSeamPix + i) * 256 + threadIdx.x;
         int r = 0, c = 0;
         bool seam_r = true;
         if (idx < n_row) {
@@ -885,9 +887,12 @@ hipError_t launch_seam(const fftsplit_plan_s& p, const float* aux, const float* 
     const int nsc = below(p.prob.w + p.P) - below(p.P);
     const long long count = (long long)nsr * p.prob.w + (long long)(p.prob.h - nsr) * nsc;
     const long long per_block = 256LL * kSeamPix;
-    const dim3 sgrid(unsigned(count > 0 ? (count + per_block - 1) / per_block : 1), unsigned(p.prob.n * p.prob.cout));
-    return launch_kernel(seam_kernel, sgrid, dim3(256), 0, s, nullptr, stop, aux, bias, y, p.prob.cout, p.prob.h,
-                         p.prob.w, p.T, p.P, p.L, p.th, p.tw, p.ntp, int(p.relu), nsr, nsc);
+    const long long bpp = count > 0 ? (count + per_block - 1) / per_block : 1;
+    const long long blocks = bpp * p.prob.n * p.prob.cout;
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    return launch_kernel(seam_kernel, dim3(unsigned(blocks)), dim3(256), 0, s, nullptr, stop, aux, bias, y,
+                         p.prob.cout, p.prob.h, p.prob.w, p.T, p.P, p.L, p.th, p.tw, p.ntp, int(p.relu), nsr, nsc,
+                         int(bpp));
 }
 
 template <int L, int TG>
