@@ -307,7 +307,8 @@ __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux
 //     executes two paths;
 //   * the crops (T x T tiles, eq. 10) are placed in an LDS band of whole
 //     output rows (band.hpp, no halo; pitch `obp`, odd) and the band is
-//     written with 16-byte stores, lanes along each row, with bias and ReLU;
+//     written with 16-byte streaming stores (kStoreStream: no later kernel
+//     of the convolution reads y), lanes along each row, with bias and ReLU;
 //     in the first and last tile row of an item only the columns of its own
 //     tiles are written;
 //   * LDS strides are odd, so the lanes of a wave spread over the banks.
@@ -647,7 +648,7 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
 #pragma unroll
                     for (int i = 0; i < SB && k0 + i < NP; ++i) {
                         const int k = k0 + i;
-                        buf_store_f32x2(v[i], ryo, full[i] ? voff : kOutOfRange, unsigned(k * slot_step * wp * 4));
+                        buf_store_f32x2<kStoreStream>(v[i], ryo, full[i] ? voff : kOutOfRange, unsigned(k * slot_step * wp * 4));
                         rr += drp;
                         voff += dq_off;
                         const bool carry = rr >= hp;
@@ -671,8 +672,8 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
                     if (lane_ok && ps < pslots && !full && col + 2 > lo && col < hi) {
                         const float2 ve = pool4(src + 2 * k * slot_step * obp);
                         const unsigned soff = unsigned(k * slot_step * wp * 4);
-                        buf_store_f32(ve.x, ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
-                        buf_store_f32(ve.y, ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
+                        buf_store_f32<kStoreStream>(ve.x, ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
+                        buf_store_f32<kStoreStream>(ve.y, ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
                     }
                     rr += drp;
                     voff += dq_off;
@@ -746,7 +747,7 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
 #pragma unroll
                     for (int i = 0; i < SB && k0 + i < NV; ++i) {
                         const int k = k0 + i;
-                        buf_store_f32x4(v[i], ryo, full[i] ? voff : kOutOfRange, unsigned(k * slot_step * w * 4));
+                        buf_store_f32x4<kStoreStream>(v[i], ryo, full[i] ? voff : kOutOfRange, unsigned(k * slot_step * w * 4));
                         rr += dr;
                         voff += dq_off;
                         const bool carry = rr >= h;
@@ -772,10 +773,10 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
                     if (lane_ok && sl < g.slots && !full && col + 4 > lo && col < hi) {
                         const float* se = src + k * slot_step * obp;
                         const unsigned soff = unsigned(k * slot_step * w * 4);
-                        buf_store_f32(se[0], ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
-                        buf_store_f32(se[1], ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
-                        buf_store_f32(se[2], ryo, col + 2 >= lo && col + 2 < hi ? voff + 8u : kOutOfRange, soff);
-                        buf_store_f32(se[3], ryo, col + 3 >= lo && col + 3 < hi ? voff + 12u : kOutOfRange, soff);
+                        buf_store_f32<kStoreStream>(se[0], ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
+                        buf_store_f32<kStoreStream>(se[1], ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
+                        buf_store_f32<kStoreStream>(se[2], ryo, col + 2 >= lo && col + 2 < hi ? voff + 8u : kOutOfRange, soff);
+                        buf_store_f32<kStoreStream>(se[3], ryo, col + 3 >= lo && col + 3 < hi ? voff + 12u : kOutOfRange, soff);
                     }
                     rr += dr;
                     voff += dq_off;

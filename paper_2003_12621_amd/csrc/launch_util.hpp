@@ -79,6 +79,11 @@ __device__ __forceinline__ float2 buf_load_f32x2(BufRsrc r, unsigned voff, unsig
 __device__ __forceinline__ float4 buf_load_f32x4(BufRsrc r, unsigned voff, unsigned soff) {
     return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
+// Cache policy of a buffer store: kStoreDefault, or kStoreStream (the "nt"
+// bit) for output that no later kernel of the same convolution reads, so
+// that it does not displace data a following kernel still needs.
+constexpr int kStoreDefault = 0;
+constexpr int kStoreStream = 2;
 // A store of more than 8 bytes needs one wait state before a VALU
 // instruction may overwrite its data registers.  The compiler's hazard model
 // assumes the wait is only needed when the scalar offset is not a register,
@@ -87,16 +92,19 @@ __device__ __forceinline__ float4 buf_load_f32x4(BufRsrc r, unsigned voff, unsig
 // uniform offset is therefore added to the lane offset and the scalar
 // offset is the constant 0, for which the compiler inserts the wait.
 // (`soff` + an out-of-range `voff` stays out of range: both are below 2^31.)
+template <int CP = kStoreDefault>
 __device__ __forceinline__ void buf_store_f32x4(float4 v, BufRsrc r, unsigned voff, unsigned soff) {
     typedef int int4v __attribute__((ext_vector_type(4)));
-    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(int4v, v), r, voff + soff, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(int4v, v), r, voff + soff, 0, CP);
 }
+template <int CP = kStoreDefault>
 __device__ __forceinline__ void buf_store_f32(float v, BufRsrc r, unsigned voff, unsigned soff) {
-    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, voff, soff, 0);
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, voff, soff, CP);
 }
+template <int CP = kStoreDefault>
 __device__ __forceinline__ void buf_store_f32x2(float2 v, BufRsrc r, unsigned voff, unsigned soff) {
     typedef int int2v __attribute__((ext_vector_type(2)));
-    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(int2v, v), r, voff, soff, 0);
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(int2v, v), r, voff, soff, CP);
 }
 
 // Optional timing events of one entry-point call: `start` is recorded when
