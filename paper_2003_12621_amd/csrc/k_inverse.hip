@@ -300,14 +300,15 @@ __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux
 // of 4, at most 256; crop width T >= L/2).  Same work items and transforms as inverse_kernel;
 // what changes is the memory traffic and how items overlap:
 //   * the output spectra of item i+1 are loaded into registers while item
-//     i is transformed and stored;
+//     i is transformed and stored (streaming loads: nothing reads them
+//     again);
 //   * the column pass runs one instruction stream in every lane: lane j = 0,
 //     which rebuilds the two Hermitian columns k2 = 0 and k2 = L/2 and packs
 //     them as one complex sequence, does so with selects, so no wave
 //     executes two paths;
 //   * the crops (T x T tiles, eq. 10) are placed in an LDS band of whole
 //     output rows (band.hpp, no halo; pitch `obp`, odd) and the band is
-//     written with 16-byte streaming stores (kStoreStream: no later kernel
+//     written with 16-byte streaming stores (kCacheStream: no later kernel
 //     of the convolution reads y), lanes along each row, with bias and ReLU;
 //     in the first and last tile row of an item only the columns of its own
 //     tiles are written;
@@ -426,12 +427,12 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
         const unsigned vb0 = ok ? lane8 + unsigned(j0 ? bin_real_b(L) : bin_mid(L, H2, jc)) * bs8 : kOutOfRange;
         const unsigned va = ok ? lane8 + unsigned(j0 ? bin_col0(L, 1) - 1 : bin_mid(L, 0, jc)) * bs8 : kOutOfRange;
         const unsigned vb = ok ? lane8 + unsigned(j0 ? bin_colh(L, 1) - 1 : bin_mid(L, H2, jc)) * bs8 : kOutOfRange;
-        pa[0] = buf_load_f32x2(ry, va0, 0);
-        pb[0] = buf_load_f32x2(ry, vb0, 0);
+        pa[0] = buf_load_f32x2<kCacheStream>(ry, va0, 0);
+        pb[0] = buf_load_f32x2<kCacheStream>(ry, vb0, 0);
 #pragma unroll
         for (int k1 = 1; k1 < H2; ++k1) {
-            pa[k1] = buf_load_f32x2(ry, va, unsigned(k1) * bs8);
-            pb[k1] = buf_load_f32x2(ry, vb, unsigned(k1) * bs8);
+            pa[k1] = buf_load_f32x2<kCacheStream>(ry, va, unsigned(k1) * bs8);
+            pb[k1] = buf_load_f32x2<kCacheStream>(ry, vb, unsigned(k1) * bs8);
         }
     };
 
@@ -648,7 +649,7 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
 #pragma unroll
                     for (int i = 0; i < SB && k0 + i < NP; ++i) {
                         const int k = k0 + i;
-                        buf_store_f32x2<kStoreStream>(v[i], ryo, full[i] ? voff : kOutOfRange, unsigned(k * slot_step * wp * 4));
+                        buf_store_f32x2<kCacheStream>(v[i], ryo, full[i] ? voff : kOutOfRange, unsigned(k * slot_step * wp * 4));
                         rr += drp;
                         voff += dq_off;
                         const bool carry = rr >= hp;
@@ -672,8 +673,8 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
                     if (lane_ok && ps < pslots && !full && col + 2 > lo && col < hi) {
                         const float2 ve = pool4(src + 2 * k * slot_step * obp);
                         const unsigned soff = unsigned(k * slot_step * wp * 4);
-                        buf_store_f32<kStoreStream>(ve.x, ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
-                        buf_store_f32<kStoreStream>(ve.y, ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
+                        buf_store_f32<kCacheStream>(ve.x, ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
+                        buf_store_f32<kCacheStream>(ve.y, ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
                     }
                     rr += drp;
                     voff += dq_off;
@@ -747,7 +748,7 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
 #pragma unroll
                     for (int i = 0; i < SB && k0 + i < NV; ++i) {
                         const int k = k0 + i;
-                        buf_store_f32x4<kStoreStream>(v[i], ryo, full[i] ? voff : kOutOfRange, unsigned(k * slot_step * w * 4));
+                        buf_store_f32x4<kCacheStream>(v[i], ryo, full[i] ? voff : kOutOfRange, unsigned(k * slot_step * w * 4));
                         rr += dr;
                         voff += dq_off;
                         const bool carry = rr >= h;
@@ -773,10 +774,10 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
                     if (lane_ok && sl < g.slots && !full && col + 4 > lo && col < hi) {
                         const float* se = src + k * slot_step * obp;
                         const unsigned soff = unsigned(k * slot_step * w * 4);
-                        buf_store_f32<kStoreStream>(se[0], ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
-                        buf_store_f32<kStoreStream>(se[1], ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
-                        buf_store_f32<kStoreStream>(se[2], ryo, col + 2 >= lo && col + 2 < hi ? voff + 8u : kOutOfRange, soff);
-                        buf_store_f32<kStoreStream>(se[3], ryo, col + 3 >= lo && col + 3 < hi ? voff + 12u : kOutOfRange, soff);
+                        buf_store_f32<kCacheStream>(se[0], ryo, col >= lo && col < hi ? voff : kOutOfRange, soff);
+                        buf_store_f32<kCacheStream>(se[1], ryo, col + 1 >= lo && col + 1 < hi ? voff + 4u : kOutOfRange, soff);
+                        buf_store_f32<kCacheStream>(se[2], ryo, col + 2 >= lo && col + 2 < hi ? voff + 8u : kOutOfRange, soff);
+                        buf_store_f32<kCacheStream>(se[3], ryo, col + 3 >= lo && col + 3 < hi ? voff + 12u : kOutOfRange, soff);
                     }
                     rr += dr;
                     voff += dq_off;

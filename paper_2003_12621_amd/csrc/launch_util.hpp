@@ -69,21 +69,24 @@ __device__ __forceinline__ uint4 load_stream_u4(const uint4* p) {
     return make_uint4(t.x, t.y, t.z, t.w);
 }
 
+// Cache policy of a buffer load or store: kCacheDefault, or kCacheStream
+// (the "nt" bit) for data that no later kernel of the same convolution
+// reads (an input the stage consumes for good, or the layer's output), so
+// that it does not displace data a following kernel still needs.
+constexpr int kCacheDefault = 0;
+constexpr int kCacheStream = 2;
+
 __device__ __forceinline__ float buf_load_f32(BufRsrc r, unsigned voff, unsigned soff) {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
 }
+template <int CP = kCacheDefault>
 __device__ __forceinline__ float2 buf_load_f32x2(BufRsrc r, unsigned voff, unsigned soff) {
     typedef int int2v __attribute__((ext_vector_type(2)));
-    return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+    return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, CP));
 }
 __device__ __forceinline__ float4 buf_load_f32x4(BufRsrc r, unsigned voff, unsigned soff) {
     return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
-// Cache policy of a buffer store: kStoreDefault, or kStoreStream (the "nt"
-// bit) for output that no later kernel of the same convolution reads, so
-// that it does not displace data a following kernel still needs.
-constexpr int kStoreDefault = 0;
-constexpr int kStoreStream = 2;
 // A store of more than 8 bytes needs one wait state before a VALU
 // instruction may overwrite its data registers.  The compiler's hazard model
 // assumes the wait is only needed when the scalar offset is not a register,
@@ -92,16 +95,16 @@ constexpr int kStoreStream = 2;
 // uniform offset is therefore added to the lane offset and the scalar
 // offset is the constant 0, for which the compiler inserts the wait.
 // (`soff` + an out-of-range `voff` stays out of range: both are below 2^31.)
-template <int CP = kStoreDefault>
+template <int CP = kCacheDefault>
 __device__ __forceinline__ void buf_store_f32x4(float4 v, BufRsrc r, unsigned voff, unsigned soff) {
     typedef int int4v __attribute__((ext_vector_type(4)));
     __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(int4v, v), r, voff + soff, 0, CP);
 }
-template <int CP = kStoreDefault>
+template <int CP = kCacheDefault>
 __device__ __forceinline__ void buf_store_f32(float v, BufRsrc r, unsigned voff, unsigned soff) {
     __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, voff, soff, CP);
 }
-template <int CP = kStoreDefault>
+template <int CP = kCacheDefault>
 __device__ __forceinline__ void buf_store_f32x2(float2 v, BufRsrc r, unsigned voff, unsigned soff) {
     typedef int int2v __attribute__((ext_vector_type(2)));
     __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(int2v, v), r, voff, soff, CP);
