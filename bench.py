@@ -5,13 +5,23 @@ Default workload: the 56x56x256 layer with a 5x5 kernel, batch 16,
 L = 32), overlap-save; synthetic seeded inputs (ReLU of N(0,1)) and
 He-normal weights, resident in device memory before timing starts.
 
-A step is one pass of the hot path over the batch: forward patch
-transform -> per-bin contraction -> inverse transform with placement (the
-three kernels of fftsplit_conv2d, launched through the stage entry points
-so that each can be timed with events on the stream it runs on).  The
-filter spectra are computed once, before timing (a once-per-layer cost).
+A step is one pass of the hot path over the batch: one fftsplit_conv2d call
+(forward patch transform -> per-bin contraction -> inverse transform with
+placement).  The filter spectra are computed once, before timing (a
+once-per-layer cost).
 
-Prints one JSON line (see the fields below).
+Order of a run: an untimed clock-settle pre-roll (steps for --settle-s
+seconds, reported as settle_s / settle_steps: a GPU given only a few
+milliseconds of work is still raising its clocks), then --warmup counted
+warm-up steps, then exactly --steps timed steps between two events on the
+launch stream, synchronised on both sides.  Per-kernel times come from a
+separate pass of the same steps made of the three stage calls.
+
+Prints one JSON line.  Besides the headline layer it carries, under
+"workloads", settled step times and stage fractions of the other single
+layers (1x3x32^2 -> 16 K3; 1x64x224^2 -> 64 K3 at T = 6/14/30;
+8x128x112^2 -> 128 K3 at T = 14/30; the headline layer at T = 12) and of
+the VGG-16 stack at batch 32.
 """
 from __future__ import annotations
 
@@ -32,29 +42,68 @@ FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix, TFLOP/s
 
 DEFAULT_CONFIG = "c4_56x256_k5"
 DEFAULT_TILE = 28
-WARMUP_S = 1.0                 # default warm-up: seconds of untimed steps
+SETTLE_S = 1.0                 # untimed clock-settle pre-roll, seconds
+DEFAULT_WARMUP = 10
+DEFAULT_STEPS = 100
+
+# the other workloads reported beside the headline layer: (config, tile)
+OTHER_LAYERS = [("c1_32x3", 6), ("c2_224x64", 6), ("c2_224x64", 14), ("c2_224x64", 30),
+                ("c3_112x128", 14), ("c3_112x128", 30), ("c4_56x256_k5", 12)]
 
 
-def warm_up(step, warmup, min_s=WARMUP_S):
-    """Untimed steps before timing: `warmup` of them if given, else as many
-    as fill `min_s` seconds (at least 10), so that the GPU's clocks have
-    settled (a few milliseconds of work measure a GPU still ramping up).
-    Returns the number of steps run."""
+def _sync():
     import torch
-    if warmup is not None:
-        for _ in range(warmup):
-            step()
-        torch.cuda.synchronize()
-        return warmup
+    torch.cuda.synchronize()
+
+
+def settle(step, seconds):
+    """Untimed steps until `seconds` have passed (batches of 10), so that the
+    GPU's clocks have settled.  Returns (steps run, seconds spent)."""
+    if seconds <= 0:
+        return 0, 0.0
     n = 0
     t0 = time.perf_counter()
     while True:
         for _ in range(10):
             step()
         n += 10
-        torch.cuda.synchronize()
-        if time.perf_counter() - t0 >= min_s:
-            return n
+        _sync()
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            return n, el
+
+
+def warm_up(step, count):
+    for _ in range(count):
+        step()
+    _sync()
+
+
+def timed_steps(step, steps):
+    """Exactly `steps` calls between two events on the current stream,
+    synchronised on both sides; returns (ms per step, wall seconds)."""
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    _sync()
+    t = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    _sync()
+    return e0.elapsed_time(e1) / steps, time.perf_counter() - t
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 def algorithmic_counts(layer, info):
@@ -66,7 +115,7 @@ def algorithmic_counts(layer, info):
               two real bins, per (patch, input channel, output channel)
     inverse : read the output spectra once + write y once
     """
-    F, ntp, coutp = info.bins, info.tiles_padded, info.cout_padded
+    F = info.bins
     nt = info.tiles
     x_bytes = 4 * layer.n * layer.cin * layer.h * layer.w
     y_bytes = 4 * layer.n * layer.cout * layer.h * layer.w
@@ -104,11 +153,12 @@ def cpu_baseline(layer, x, w, b, tile, budget_s=12.0):
         d_total += time.perf_counter() - t0
         d_done += 1
     d_img = d_total / d_done
+    model = cpu_model()
     return {"value": round(gflops, 3), "unit": "GFLOP/s", "cores": int(min(cores, blas_threads)),
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": model,
             "sample": f"oracle.split_conv (float64 numpy, naive-DFT split, overlap-save) on {done} of "
                       f"{layer.n} images, {t_total:.1f} s; {1.0 / per_img:.3f} images/s; "
-                      f"{cores} host cores visible, BLAS threads {blas_threads}",
+                      f"{cores} host cores visible ({model}), BLAS threads {blas_threads}",
             "direct_xcorr2d": {"value": round(layer.direct_flops / layer.n / d_img / 1e9, 3), "unit": "GFLOP/s",
                                "sample": f"oracle.direct_xcorr2d (float64 numpy, K*K shifted tensordots) on "
                                          f"{d_done} of {layer.n} images, {d_total:.1f} s; "
@@ -134,11 +184,178 @@ def load_traffic(kernel, workload_tag):
         return None
 
 
-def bench_vgg16(args):
-    """The 13-layer VGG-16 stack at batch 32 (3x224x224 -> 512x7x7), each
-    layer's tile chosen by its plan; a step is one forward of the stack."""
+class LayerRun:
+    """One layer's plan, filter spectra, workspace and output, with the
+    inputs resident on the device."""
+
+    def __init__(self, layer, x, w, b, tile, mode, dev):
+        import torch
+        import paper_2003_12621_amd as fs
+        self.fs = fs
+        self.layer = layer
+        self.plan = fs.Plan(layer.n, layer.cin, layer.h, layer.w, layer.cout, layer.k, tile=tile, mode=mode,
+                            bias=b is not None, device=dev.index)
+        self.info = self.plan.info
+        self.xd = torch.from_numpy(x).to(dev)
+        self.wd = torch.from_numpy(w).to(dev)
+        self.bd = None if b is None else torch.from_numpy(b).to(dev)
+        self.wspec = self.plan.transform_weights(self.wd)
+        self.ws = self.plan.new_workspace()
+        self.y = self.plan.new_output()
+        _sync()
+
+    def step(self):
+        # one pass of the path: the library's single-call entry point
+        self.plan.conv2d(self.xd, self.wspec, self.bd, out=self.y, workspace=self.ws)
+
+    def stage_times(self, steps):
+        """Per-kernel durations over `steps` passes made of the three stage
+        calls, each kernel's (start, stop) recorded from its own dispatch
+        timestamps (fftsplit_set_timing_events).  Timing every launch
+        lengthens the gaps between kernels, not the kernels."""
+        import torch
+        fs, plan = self.fs, self.plan
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(steps)]
+        for row in evs:          # give every event its device handle
+            for e in row:
+                e.record()
+        _sync()
+        for ev in evs:
+            fs.set_timing_events(ev[0], ev[1])
+            plan.forward(self.xd, self.ws)
+            fs.set_timing_events(ev[2], ev[3])
+            plan.contract(self.wspec, self.ws)
+            fs.set_timing_events(ev[4], ev[5])
+            plan.inverse(self.ws, bias=self.bd, out=self.y)
+            fs.set_timing_events()
+        _sync()
+        fwd = [e[0].elapsed_time(e[1]) for e in evs]
+        con = [e[2].elapsed_time(e[3]) for e in evs]
+        inv = [e[4].elapsed_time(e[5]) for e in evs]
+        staged = evs[0][0].elapsed_time(evs[-1][5]) / steps
+        return fwd, con, inv, staged
+
+    def cold_stage_times(self, steps):
+        """Stage times with a cold last-level cache: before every stage a
+        512 MB buffer is read (summed), which fills the 256 MB cache with
+        clean lines, so each stage reads its inputs from HBM."""
+        import torch
+        fs, plan = self.fs, self.plan
+        flush = torch.ones(128 << 20, dtype=torch.float32, device=self.xd.device)   # 512 MB
+        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(steps)]
+        for row in cev:
+            for e in row:
+                e.record()
+        _sync()
+        for ev in cev:
+            flush.sum()
+            fs.set_timing_events(ev[0], ev[1])
+            plan.forward(self.xd, self.ws)
+            fs.set_timing_events()
+            flush.sum()
+            fs.set_timing_events(ev[2], ev[3])
+            plan.contract(self.wspec, self.ws)
+            fs.set_timing_events()
+            flush.sum()
+            fs.set_timing_events(ev[4], ev[5])
+            plan.inverse(self.ws, bias=self.bd, out=self.y)
+            fs.set_timing_events()
+        _sync()
+        del flush
+        return [sum(e[2 * j].elapsed_time(e[2 * j + 1]) for e in cev) / steps for j in range(3)]
+
+    def parity(self, x, w, b, images, channels):
+        """rel-L2 of the last output against the oracle on the given images
+        and output channels."""
+        import oracle
+        ref = oracle.direct_xcorr2d(x[images], w[channels], None if b is None else b[channels])
+        got = self.y.cpu().numpy()[images][:, channels].astype(np.float64)
+        return float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+
+
+def _avg(v):
+    return sum(v) / len(v)
+
+
+def stage_record(counts, fwd, con, inv):
+    fwd_gbs = counts["forward_bytes"] / (fwd * 1e-3) / 1e9
+    inv_gbs = counts["inverse_bytes"] / (inv * 1e-3) / 1e9
+    con_tfs = counts["contract_flops"] / (con * 1e-3) / 1e12
+    return {
+        "forward": {"ms": round(fwd, 4), "GB/s": round(fwd_gbs, 1), "frac_hbm": round(fwd_gbs / HBM_PEAK_GBS, 4),
+                    "bytes": counts["forward_bytes"]},
+        "contract": {"ms": round(con, 4), "TFLOP/s": round(con_tfs, 2),
+                     "frac_mfma": round(con_tfs / FP32_MFMA_PEAK_TFLOPS, 4), "flops": counts["contract_flops"],
+                     "bytes": counts["contract_bytes"]},
+        "inverse": {"ms": round(inv, 4), "GB/s": round(inv_gbs, 1), "frac_hbm": round(inv_gbs / HBM_PEAK_GBS, 4),
+                    "bytes": counts["inverse_bytes"]},
+    }
+
+
+def other_layer(name, tile, dev, steps=20, settle_s=0.25):
+    """A short settled measurement of another single layer: step time,
+    effective GFLOP/s, images/s and stage fractions, and the oracle's
+    rel-L2 on a sample of the output."""
+    from workloads import CONFIGS, make_config
+    layer = CONFIGS[name]["layer"]
+    x, w, b = make_config(name)
+    run = LayerRun(layer, x, w, b, tile, "os", dev)
+    settle(run.step, settle_s)
+    warm_up(run.step, 5)
+    ms, _ = timed_steps(run.step, steps)
+    fwd, con, inv, _ = run.stage_times(steps)
+    counts = algorithmic_counts(layer, run.info)
+    chans = sorted({0, layer.cout // 2, layer.cout - 1})
+    rec = {"workload": f"n={layer.n} cin={layer.cin} {layer.h}x{layer.w} cout={layer.cout} k={layer.k}",
+           "tile": run.info.tile, "nfft": run.info.nfft, "steps": steps, "ms_per_step": round(ms, 4),
+           "GFLOP/s": round(layer.direct_flops / (ms * 1e-3) / 1e9, 1),
+           "images_per_s": round(layer.n / (ms * 1e-3), 1),
+           "stages": stage_record(counts, _avg(fwd), _avg(con), _avg(inv)),
+           "fused_channel_sum": bool(run.info.fused_channel_sum),
+           "parity_rel_l2": run.parity(x, w, b, slice(0, 1), chans)}
+    del run
+    return rec
+
+
+def vgg16_summary(dev, steps=10, settle_s=0.5):
+    """The VGG-16 stack at batch 32 (plan-chosen tiles, fused max-pools):
+    settled step time, effective GFLOP/s, images/s, per-layer times."""
     import torch
-    import paper_2003_12621_amd as fs  # noqa: F401
+    from paper_2003_12621_amd.vgg import VGG16Stack
+    from workloads import VGG16_LAYERS, VGG_BATCH, make_vgg16
+    x, layers = make_vgg16(batch=VGG_BATCH, seed=0)
+    stack = VGG16Stack(layers, batch=VGG_BATCH)
+    xd = torch.from_numpy(x).to(dev)
+    fwd = lambda: stack.forward(xd)  # noqa: E731
+    settle(fwd, settle_s)
+    warm_up(fwd, 3)
+    ms, _ = timed_steps(fwd, steps)
+    flops = sum(2 * VGG_BATCH * cout * hw * hw * cin * 9 for cin, cout, hw in VGG16_LAYERS)
+    reps = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(13)]
+            for _ in range(steps)]
+    for row in reps:
+        for a, b in row:
+            a.record()
+            b.record()
+    _sync()
+    for row in reps:
+        stack.forward(xd, layer_events=row)
+    _sync()
+    layer_ms = [round(sum(r[i][0].elapsed_time(r[i][1]) for r in reps) / steps, 4) for i in range(13)]
+    # final activation of image 0 against the float64 chain
+    import oracle
+    got = stack.forward(xd)[:1].cpu().numpy().astype(np.float64)
+    ref = oracle.vgg16_forward(x[:1], layers)
+    return {"workload": f"vgg16 conv stack, batch {VGG_BATCH}, 3x224x224, bias+ReLU, 5 max-pools",
+            "tiles": stack.tiles, "steps": steps, "ms_per_step": round(ms, 4),
+            "GFLOP/s": round(flops / (ms * 1e-3) / 1e9, 1), "images_per_s": round(VGG_BATCH / (ms * 1e-3), 1),
+            "layer_ms": layer_ms,
+            "parity_rel_l2_image0": float(np.linalg.norm(got - ref) / np.linalg.norm(ref))}
+
+
+def bench_vgg16(args):
+    """--config vgg16: the 13-layer VGG-16 stack at batch 32 as the step."""
+    import torch
     from paper_2003_12621_amd.vgg import VGG16Stack
     from workloads import VGG16_LAYERS, VGG_BATCH, make_vgg16
     dev = torch.device("cuda", 0)
@@ -146,50 +363,22 @@ def bench_vgg16(args):
     x, layers = make_vgg16(batch=VGG_BATCH, seed=0)
     stack = VGG16Stack(layers, batch=VGG_BATCH, mode=args.mode)
     xd = torch.from_numpy(x).to(dev)
-    args.warmup = warm_up(lambda: stack.forward(xd), args.warmup)
-    args.steps = args.steps or 20
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
-        stack.forward(xd)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
-    flops = 0
-    for i, (cin, cout, hw) in enumerate(VGG16_LAYERS, start=1):
-        flops += 2 * VGG_BATCH * cout * hw * hw * cin * 9
-    # per-layer times: further passes with each layer's convolution call
-    # timed from its kernels' dispatch timestamps (max-pools included where
-    # a layer ends a stage)
-    reps = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(13)]
-            for _ in range(args.steps)]
-    for row in reps:
-        for a, b in row:
-            a.record()
-            b.record()
-    torch.cuda.synchronize()
-    for row in reps:
-        stack.forward(xd, layer_events=row)
-    torch.cuda.synchronize()
-    per_layer = []
-    for i, (cin, cout, hw) in enumerate(VGG16_LAYERS):
-        lms = sum(r[i][0].elapsed_time(r[i][1]) for r in reps) / len(reps)
-        plan = stack.plans[i]
-        per_layer.append({"layer": i + 1, "cin": cin, "cout": cout, "hw": hw, "tile": plan.tile,
-                          "pool": bool(plan.pool), "fused_channel_sum": bool(plan.info.fused_channel_sum),
-                          "ms": round(lms, 4),
-                          "GFLOP/s": round(2 * VGG_BATCH * cout * hw * hw * cin * 9 / (lms * 1e-3) / 1e9, 1)})
-    spatial = None
-    if not args.no_compare:
-        spatial = time_vgg_spatial(args, layers, x, stack)
+    step = lambda: stack.forward(xd)  # noqa: E731
+    settle_n, settle_s = settle(step, args.settle_s)
+    warm_up(step, args.warmup)
+    steps = args.steps or 20
+    ms, wall = timed_steps(step, steps)
+    flops = sum(2 * VGG_BATCH * cout * hw * hw * cin * 9 for cin, cout, hw in VGG16_LAYERS)
     out = {"metric": "effective direct-conv GFLOP/s", "value": round(flops / (ms * 1e-3) / 1e9, 1),
-           "unit": "GFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "unit": "GFLOP/s", "n_gpus": 1, "steps": steps, "warmup": args.warmup,
            "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": "f32", "data": "synthetic",
            "config": {"workload": f"vgg16 conv stack, batch {VGG_BATCH}, 3x224x224, bias+ReLU, 5 max-pools",
                       "tiles": stack.tiles, "mode": args.mode},
-           "images_per_s": round(VGG_BATCH / (ms * 1e-3), 1), "layers": per_layer}
-    if spatial is not None:
+           "images_per_s": round(VGG_BATCH / (ms * 1e-3), 1), "settle_s": round(settle_s, 3),
+           "settle_steps": settle_n, "wall_s_timed": round(wall, 4)}
+    if not args.no_compare:
+        spatial = time_vgg_spatial(args, layers, x, stack)
         for v in spatial.values():
             if isinstance(v, dict):
                 v["GFLOP/s"] = round(flops / (v["ms"] * 1e-3) / 1e9, 1)
@@ -222,20 +411,16 @@ def time_vgg_spatial(args, layers, x, split_stack):
 
     res = {}
     oaa = VGG16Stack(layers, batch=VGG_BATCH, tiles=[3] * 13, mode="oaa")
+    steps = args.steps or 20
     for name, fn in (("direct_hip", lambda: direct.forward(xd)), ("torch_conv2d", torch_stack),
                      ("oaaconv", lambda: oaa.forward(xd))):
-        warm_up(fn, None, min_s=0.3)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(args.steps):
-            fn()
-        e1.record()
-        torch.cuda.synchronize()
-        res[name] = {"ms": round(e0.elapsed_time(e1) / args.steps, 4)}
+        settle(fn, 0.3)
+        ms, _ = timed_steps(fn, steps)
+        res[name] = {"ms": round(ms, 4)}
     ys = split_stack.forward(xd).clone()
     yd = direct.forward(xd).clone()
     yt = torch_stack()
-    torch.cuda.synchronize()
+    _sync()
     nt = torch.linalg.vector_norm(yt)
     res["direct_hip"]["rel_l2_vs_torch"] = float(torch.linalg.vector_norm(yd - yt) / nt)
     res["split_rel_l2_vs_torch"] = float(torch.linalg.vector_norm(ys - yt) / nt)
@@ -243,12 +428,75 @@ def time_vgg_spatial(args, layers, x, split_stack):
     return res
 
 
+def time_oaaconv(steps, layer, xd, wd, bd):
+    """The same layer by OaAConv, the paper's comparison method (Section 2,
+    Fig. 1): this library's overlap-add pipeline at T = K, L = 2K - 1, timed
+    like the split path (conv2d steps; stage times from a staged pass)."""
+    import torch
+    import paper_2003_12621_amd as fs
+    k = layer.k
+    plan = fs.Plan(layer.n, layer.cin, layer.h, layer.w, layer.cout, k, tile=k, mode="oaa", bias=bd is not None,
+                   device=0)
+    wspec = plan.transform_weights(wd)
+    ws = plan.new_workspace()
+    y = plan.new_output()
+    step = lambda: plan.conv2d(xd, wspec, bd, out=y, workspace=ws)  # noqa: E731
+    settle(step, 0.3)
+    ms, _ = timed_steps(step, steps)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    for e in ev:
+        e.record()
+    _sync()
+    fs.set_timing_events(ev[0], ev[1])
+    plan.forward(xd, ws)
+    fs.set_timing_events(ev[2], ev[3])
+    plan.contract(wspec, ws)
+    fs.set_timing_events(ev[4], ev[5])
+    plan.inverse(ws, bias=bd, out=y)
+    fs.set_timing_events()
+    _sync()
+    info = plan.info
+    return {"ms": round(ms, 4), "GFLOP/s": round(layer.direct_flops / (ms * 1e-3) / 1e9, 1),
+            "tile": info.tile, "nfft": info.nfft, "tiles": info.tiles, "bins": info.bins,
+            "contract_flops": (8 * info.bins) * layer.cin * layer.cout * info.tiles,
+            "stage_ms": {"forward": round(ev[0].elapsed_time(ev[1]), 4),
+                         "contract": round(ev[2].elapsed_time(ev[3]), 4),
+                         "inverse_and_seams": round(ev[4].elapsed_time(ev[5]), 4)}}
+
+
+def time_spatial_methods(steps, run):
+    """The same layer by spatial convolution, timed the same way (context for
+    the split method's speed, as the paper sets it beside direct convolution):
+    this library's direct kernel (fftsplit_direct_conv2d) and torch's fp32
+    conv2d (MIOpen), both on torch's current stream."""
+    import torch
+    import torch.nn.functional as F
+
+    torch.backends.cudnn.allow_tf32 = False
+    plan, layer, xd, wd, bd = run.plan, run.layer, run.xd, run.wd, run.bd
+    wdir = plan.direct_transform_weights(wd)
+    yd = plan.new_output()
+    res = {}
+    runs = {"direct_hip": lambda: plan.direct_conv2d(xd, wdir, bd, out=yd),
+            "torch_conv2d": lambda: F.conv2d(xd, wd, bd, padding=layer.k // 2)}
+    for name, fn in runs.items():
+        settle(fn, 0.3)
+        ms, _ = timed_steps(fn, steps)
+        res[name] = {"ms": round(ms, 4), "GFLOP/s": round(layer.direct_flops / (ms * 1e-3) / 1e9, 1)}
+    yt = F.conv2d(xd, wd, bd, padding=layer.k // 2)
+    _sync()
+    res["direct_hip"]["rel_l2_vs_torch"] = float(torch.linalg.vector_norm(yd - yt) / torch.linalg.vector_norm(yt))
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=None, help="timed steps (default 100; 20 for vgg16)")
-    ap.add_argument("--warmup", type=int, default=None,
-                    help=f"untimed steps first (default: as many as fill {WARMUP_S:g} s)")
+    ap.add_argument("--steps", type=int, default=None, help=f"timed steps (default {DEFAULT_STEPS}; 20 for vgg16)")
+    ap.add_argument("--warmup", type=int, default=DEFAULT_WARMUP,
+                    help="counted warm-up steps, after the clock-settle pre-roll")
+    ap.add_argument("--settle-s", type=float, default=SETTLE_S,
+                    help="seconds of untimed steps before the warm-up (0: none)")
     ap.add_argument("--config", default=DEFAULT_CONFIG, help="a layer config name, or vgg16")
     ap.add_argument("--shape", default=None,
                     help="any layer instead of a named config: n,cin,h,w,cout,k (ReLU(N(0,1)) inputs, He weights)")
@@ -259,6 +507,8 @@ def main():
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache stage timings")
     ap.add_argument("--no-compare", action="store_true",
                     help="skip timing the spatial methods (this library's direct kernel, torch/MIOpen conv2d)")
+    ap.add_argument("--no-others", action="store_true",
+                    help="skip the other workloads (the other single layers and the VGG-16 stack)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="before timing, copy a buffer of this many MiB 3 times (calibrates HBM counters)")
     args = ap.parse_args()
@@ -269,7 +519,6 @@ def main():
         sys.exit(2)
 
     import torch
-    import paper_2003_12621_amd as fs
     from workloads import CONFIGS, make_config
 
     if args.config == "vgg16" and not args.shape:
@@ -282,140 +531,58 @@ def main():
         layer = Layer(*vals)
         args.config = "shape_" + "x".join(str(v) for v in vals)
         tile = args.tile if args.tile is not None else 0
-        make = lambda: make_layer(layer)  # noqa: E731
+        x, w, b = make_layer(layer)
     else:
         cfg = CONFIGS[args.config]
         layer = cfg["layer"]
         tile = (args.tile if args.tile is not None
                 else (DEFAULT_TILE if args.config == DEFAULT_CONFIG else cfg["tiles"][-1]))
-        make = lambda: make_config(args.config)  # noqa: E731
+        x, w, b = make_config(args.config)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
 
-    x, w, b = make()
-    plan = fs.Plan(layer.n, layer.cin, layer.h, layer.w, layer.cout, layer.k, tile=tile, mode=args.mode,
-                   bias=b is not None, device=0)
-    info = plan.info
+    run = LayerRun(layer, x, w, b, tile, args.mode, dev)
+    info = run.info
     tile = info.tile
-    xd = torch.from_numpy(x).to(dev)
-    wd = torch.from_numpy(w).to(dev)
-    bd = None if b is None else torch.from_numpy(b).to(dev)
-    wspec = plan.transform_weights(wd)
-    ws = plan.new_workspace()
-    y = plan.new_output()
     if args.copy_probe_mb > 0:
         nbytes = args.copy_probe_mb << 20
         src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
         for _ in range(3):
             dst.copy_(src)
-        torch.cuda.synchronize()
+        _sync()
         del src, dst
-    torch.cuda.synchronize()
 
-    def step():
-        # one pass of the path: the library's single-call entry point
-        plan.conv2d(xd, wspec, bd, out=y, workspace=ws)
+    settle_n, settle_s = settle(run.step, args.settle_s)
+    warm_up(run.step, args.warmup)
+    steps = args.steps or DEFAULT_STEPS
 
-    def staged_step(ev):
-        # the same pass as three stage calls, each kernel's (start, stop)
-        # recorded from its own dispatch timestamps (fftsplit_set_timing_events)
-        fs.set_timing_events(ev[0], ev[1])
-        plan.forward(xd, ws)
-        fs.set_timing_events(ev[2], ev[3])
-        plan.contract(wspec, ws)
-        fs.set_timing_events(ev[4], ev[5])
-        plan.inverse(ws, bias=bd, out=y)
-        fs.set_timing_events()
+    # Timed region: exactly `steps` conv2d calls, synchronised on both sides.
+    ms_per_step, t_wall = timed_steps(run.step, steps)
 
-    args.warmup = warm_up(step, args.warmup)
-    args.steps = args.steps or 100
-
-    # Timed region: K steps, synchronised on both sides.
-    e_start, e_stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    e_start.record()
-    for _ in range(args.steps):
-        step()
-    e_stop.record()
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    ms_per_step = e_start.elapsed_time(e_stop) / args.steps
-
-    # Per-kernel durations: K more steps with every kernel timed.  Timing
-    # events on every launch lengthen the gaps between kernels (not the
-    # kernels), so they are kept out of the region above.
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
-    for row in evs:          # give every event its device handle
-        for e in row:
-            e.record()
-    torch.cuda.synchronize()
-    for i in range(args.steps):
-        staged_step(evs[i])
-    torch.cuda.synchronize()
-    fwd = [e[0].elapsed_time(e[1]) for e in evs]
-    con = [e[2].elapsed_time(e[3]) for e in evs]
-    inv = [e[4].elapsed_time(e[5]) for e in evs]
-    ms_per_step_staged = evs[0][0].elapsed_time(evs[-1][5]) / args.steps
-    avg = lambda v: sum(v) / len(v)  # noqa: E731
-
-    # Cold-cache stage times: before every stage a 512 MB buffer is read
-    # (summed), which fills the 256 MB last-level cache with clean lines, so
-    # each stage reads its inputs from HBM (the timings above are warm: a
-    # stage may find its input there).
-    cold = None
-    if not args.no_cold:
-        flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)   # 512 MB
-        ncold = min(args.steps, 20)
-        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(ncold)]
-        for row in cev:
-            for e in row:
-                e.record()
-        torch.cuda.synchronize()
-        for i in range(ncold):
-            ev = cev[i]
-            flush.sum()
-            fs.set_timing_events(ev[0], ev[1])
-            plan.forward(xd, ws)
-            fs.set_timing_events()
-            flush.sum()
-            fs.set_timing_events(ev[2], ev[3])
-            plan.contract(wspec, ws)
-            fs.set_timing_events()
-            flush.sum()
-            fs.set_timing_events(ev[4], ev[5])
-            plan.inverse(ws, bias=bd, out=y)
-            fs.set_timing_events()
-        torch.cuda.synchronize()
-        cold = [avg([e[2 * j].elapsed_time(e[2 * j + 1]) for e in cev]) for j in range(3)]
-        del flush
+    fwd, con, inv, ms_per_step_staged = run.stage_times(steps)
+    cold = None if args.no_cold else run.cold_stage_times(min(steps, 20))
 
     counts = algorithmic_counts(layer, info)
-    fwd_gbs = counts["forward_bytes"] / (avg(fwd) * 1e-3) / 1e9
-    inv_gbs = counts["inverse_bytes"] / (avg(inv) * 1e-3) / 1e9
-    con_tfs = counts["contract_flops"] / (avg(con) * 1e-3) / 1e12
+    stages = stage_record(counts, _avg(fwd), _avg(con), _avg(inv))
+    con_tfs = stages["contract"]["TFLOP/s"]
     value = layer.direct_flops / (ms_per_step * 1e-3) / 1e9
 
-    # Parity of the timed output against the oracle on sampled output channels.
     parity = None
     if not args.no_parity:
-        import oracle
         rng = np.random.default_rng(99)
         sel = np.sort(rng.choice(layer.cout, size=4, replace=False))
-        imgs = slice(0, min(layer.n, 4))
-        ref = oracle.direct_xcorr2d(x[imgs], w[sel], None if b is None else b[sel])
-        got = y.cpu().numpy()[imgs][:, sel].astype(np.float64)
-        parity = float(np.linalg.norm(got - ref) / np.linalg.norm(ref))
+        parity = run.parity(x, w, b, slice(0, min(layer.n, 4)), sel)
 
     wtag = f"{args.config}_T{tile}_{args.mode}"
-    traffic = load_traffic("contract", wtag)
+    stages["forward"]["traffic"] = load_traffic("forward", wtag)
+    stages["inverse"]["traffic"] = load_traffic("inverse", wtag)
     out = {
         "metric": "effective direct-conv GFLOP/s",
         "value": round(value, 1),
         "unit": "GFLOP/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
@@ -430,24 +597,16 @@ def main():
                    "contract_variant": f"{info.contract_tile_m}x{info.contract_tile_n}x{info.contract_stage_k}"
                                        f"/{info.contract_real_products}M/prefetch{info.contract_prefetch}"},
         "images_per_s": round(layer.n / (ms_per_step * 1e-3), 1),
+        "settle_s": round(settle_s, 3),
+        "settle_steps": settle_n,
         "roofline": {"bound": "mfma", "kernel": "contract (per-bin complex Cin->Cout product)",
-                     "achieved": round(con_tfs, 2), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(con_tfs / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": traffic,
+                     "achieved": con_tfs, "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(con_tfs / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": load_traffic("contract", wtag),
                      "flops_per_complex_mac": 8,
                      "mfma_real_products_per_complex_mac": info.contract_real_products,
                      "mfma_executed_frac": round(con_tfs * info.contract_real_products / 4
                                                  / FP32_MFMA_PEAK_TFLOPS, 4)},
-        "stages": {
-            "forward": {"ms": round(avg(fwd), 4), "GB/s": round(fwd_gbs, 1),
-                        "frac_hbm": round(fwd_gbs / HBM_PEAK_GBS, 4), "bytes": counts["forward_bytes"],
-                        "traffic": load_traffic("forward", wtag)},
-            "contract": {"ms": round(avg(con), 4), "TFLOP/s": round(con_tfs, 2),
-                         "frac_mfma": round(con_tfs / FP32_MFMA_PEAK_TFLOPS, 4),
-                         "flops": counts["contract_flops"], "bytes": counts["contract_bytes"]},
-            "inverse": {"ms": round(avg(inv), 4), "GB/s": round(inv_gbs, 1),
-                        "frac_hbm": round(inv_gbs / HBM_PEAK_GBS, 4), "bytes": counts["inverse_bytes"],
-                        "traffic": load_traffic("inverse", wtag)},
-        },
+        "stages": stages,
         "stages_cold": None if cold is None else {
             "forward": {"ms": round(cold[0], 4), "frac_hbm": round(counts["forward_bytes"] / (cold[0] * 1e-3) / 1e9
                                                                  / HBM_PEAK_GBS, 4)},
@@ -456,90 +615,30 @@ def main():
             "inverse": {"ms": round(cold[2], 4), "frac_hbm": round(counts["inverse_bytes"] / (cold[2] * 1e-3) / 1e9
                                                                  / HBM_PEAK_GBS, 4)},
             "note": "each stage after a 512 MB read has replaced the last-level cache's contents"},
-        "timing": "ms_per_step: K fftsplit_conv2d calls between two events on the launch stream, after "
-                  "a warm-up that lets the clocks settle; stage times: K further steps as three stage calls "
-                  "with each kernel's start/stop taken from its dispatch timestamps (hipExtLaunchKernel events)",
+        "timing": "clock-settle pre-roll (settle_s, untimed), then `warmup` counted warm-up steps, then "
+                  "ms_per_step: exactly `steps` fftsplit_conv2d calls between two events on the launch stream; "
+                  "stage times: `steps` further passes as three stage calls with each kernel's start/stop "
+                  "taken from its dispatch timestamps (hipExtLaunchKernel events)",
         "ms_per_step_staged": round(ms_per_step_staged, 4),
         "wall_s_timed": round(t_wall, 4),
         "parity_rel_l2": parity,
     }
     if not args.no_compare:
-        out["spatial_methods"] = time_spatial_methods(args, plan, layer, xd, wd, bd)
-        out["oaaconv"] = time_oaaconv(args, layer, xd, wd, bd)
+        out["spatial_methods"] = time_spatial_methods(steps, run)
+        out["oaaconv"] = time_oaaconv(steps, layer, run.xd, run.wd, run.bd)
+    if not args.no_others and not args.shape:
+        del run
+        others = {}
+        for name, t in OTHER_LAYERS:
+            if name == args.config and t == tile:
+                continue
+            others[f"{name}_T{t}"] = other_layer(name, t, dev)
+            torch.cuda.empty_cache()
+        others["vgg16_b32"] = vgg16_summary(dev)
+        out["workloads"] = others
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layer, x, w, b, tile)
     print(json.dumps(out), flush=True)
-
-
-def time_oaaconv(args, layer, xd, wd, bd):
-    """The same layer by OaAConv, the paper's comparison method (Section 2,
-    Fig. 1): this library's overlap-add pipeline at T = K, L = 2K - 1, timed
-    like the split path (K conv2d steps; stage times from a staged pass)."""
-    import torch
-    import paper_2003_12621_amd as fs
-    k = layer.k
-    plan = fs.Plan(layer.n, layer.cin, layer.h, layer.w, layer.cout, k, tile=k, mode="oaa", bias=bd is not None,
-                   device=0)
-    wspec = plan.transform_weights(wd)
-    ws = plan.new_workspace()
-    y = plan.new_output()
-    warm_up(lambda: plan.conv2d(xd, wspec, bd, out=y, workspace=ws), None, min_s=0.3)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
-        plan.conv2d(xd, wspec, bd, out=y, workspace=ws)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
-    for e in ev:
-        e.record()
-    torch.cuda.synchronize()
-    fs.set_timing_events(ev[0], ev[1])
-    plan.forward(xd, ws)
-    fs.set_timing_events(ev[2], ev[3])
-    plan.contract(wspec, ws)
-    fs.set_timing_events(ev[4], ev[5])
-    plan.inverse(ws, bias=bd, out=y)
-    fs.set_timing_events()
-    torch.cuda.synchronize()
-    info = plan.info
-    return {"ms": round(ms, 4), "GFLOP/s": round(layer.direct_flops / (ms * 1e-3) / 1e9, 1),
-            "tile": info.tile, "nfft": info.nfft, "tiles": info.tiles, "bins": info.bins,
-            "contract_flops": (8 * info.bins) * layer.cin * layer.cout * info.tiles,
-            "stage_ms": {"forward": round(ev[0].elapsed_time(ev[1]), 4),
-                         "contract": round(ev[2].elapsed_time(ev[3]), 4),
-                         "inverse_and_seams": round(ev[4].elapsed_time(ev[5]), 4)}}
-
-
-def time_spatial_methods(args, plan, layer, xd, wd, bd):
-    """The same layer by spatial convolution, timed the same way (context for
-    the split method's speed, as the paper sets it beside direct convolution):
-    this library's direct kernel (fftsplit_direct_conv2d) and torch's fp32
-    conv2d (MIOpen), both on torch's current stream."""
-    import torch
-    import torch.nn.functional as F
-
-    torch.backends.cudnn.allow_tf32 = False
-    wdir = plan.direct_transform_weights(wd)
-    yd = plan.new_output()
-    res = {}
-    runs = {"direct_hip": lambda: plan.direct_conv2d(xd, wdir, bd, out=yd),
-            "torch_conv2d": lambda: F.conv2d(xd, wd, bd, padding=layer.k // 2)}
-    for name, fn in runs.items():
-        warm_up(fn, None, min_s=0.3)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(args.steps):
-            fn()
-        e1.record()
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / args.steps
-        res[name] = {"ms": round(ms, 4), "GFLOP/s": round(layer.direct_flops / (ms * 1e-3) / 1e9, 1)}
-    yt = F.conv2d(xd, wd, bd, padding=layer.k // 2)
-    torch.cuda.synchronize()
-    res["direct_hip"]["rel_l2_vs_torch"] = float(torch.linalg.vector_norm(yd - yt) / torch.linalg.vector_norm(yt))
-    return res
 
 
 if __name__ == "__main__":

@@ -156,13 +156,29 @@ typedef struct {
      * default where the tile has that variant).  The environment variable
      * FFTSPLIT_CONTRACT_PREFETCH=1..3 overrides it at plan time. */
     int contract_prefetch;
+    /* The plan's cost model for the chosen L (Section 3.2 weighs the
+     * operations and memory accesses of a patch size; here they are priced
+     * at an effective HBM rate and matrix-core rate):
+     *   model_contract_flops  = 8 * bins * cin * cout_padded * tiles_padded
+     *                           (8 flops per complex multiply-add),
+     *   model_transform_bytes = forward bytes (x read once, patch spectra
+     *                           written once) + inverse bytes (output spectra
+     *                           read once, y written once),
+     *   model_seconds         = the modelled time the tile choice minimises. */
+    double model_contract_flops;
+    double model_transform_bytes;
+    double model_seconds;
 } fftsplit_plan_info_t;
 
 /* Validate `prob` (host) and create a plan for `device` (a HIP ordinal).
+ * The paper leaves the patch size free, to be chosen from the resources of
+ * the hardware (Section 3.1, first paragraph), and weighs a patch size by
+ * its operation count and memory accesses (Section 3.2, eqs. 13-14).  Here
+ * the choice is among the FFT sizes the kernels implement.
  * Queries the device: its gcnArchName must start with "gfx950", else
  * FFTSPLIT_ERROR_ARCH.  With prob->tile == 0 the plan picks T from a cost
- * model over L = 8, 16, 32; the environment variable FFTSPLIT_TILE forces a
- * tile size.  No device memory is touched.  *out is set only on success.
+ * model over L = 8, 16, 32 (the model_* fields of fftsplit_plan_info_t);
+ * the environment variable FFTSPLIT_TILE forces a tile size.  No device memory is touched.  *out is set only on success.
  * Other environment variables read here (for experiments; the defaults are
  * the measured best): FFTSPLIT_CONTRACT_TILE (see contract_tile_m),
  * FFTSPLIT_CONTRACT_PREFETCH (see contract_prefetch),
@@ -177,6 +193,10 @@ fftsplit_status_t fftsplit_plan(const fftsplit_problem_t* prob, int device, ffts
 fftsplit_status_t fftsplit_plan_for_arch(const fftsplit_problem_t* prob, const char* arch,
                                          fftsplit_plan_t* out);
 
+/* What the plan decided (Section 3.1: patch size T and FFT size
+ * L = T + K - 1; Section 3.2: the cost that chose them), the buffer sizes
+ * and layouts the caller must provide, and the kernel variants.  Fails with
+ * FFTSPLIT_ERROR_INVALID_VALUE on a NULL argument. */
 fftsplit_status_t fftsplit_plan_info(fftsplit_plan_t plan, fftsplit_plan_info_t* out /* host */);
 
 /* Frees a plan's host memory.  NULL is ignored. */

@@ -54,7 +54,9 @@ class PlanInfo(ctypes.Structure):
                 ("contract_tile_m", ctypes.c_int), ("contract_tile_n", ctypes.c_int),
                 ("contract_stage_k", ctypes.c_int), ("contract_real_products", ctypes.c_int),
                 ("spec_group", ctypes.c_int), ("fused_channel_sum", ctypes.c_int),
-                ("direct_wspec_bytes", ctypes.c_size_t), ("contract_prefetch", ctypes.c_int)]
+                ("direct_wspec_bytes", ctypes.c_size_t), ("contract_prefetch", ctypes.c_int),
+                ("model_contract_flops", ctypes.c_double), ("model_transform_bytes", ctypes.c_double),
+                ("model_seconds", ctypes.c_double)]
 
 
 class FftsplitError(RuntimeError):
@@ -228,6 +230,15 @@ class Plan:
                "fftsplit_transform_weights")
         return out
 
+    def _wspec(self, wspec):
+        # the C ABI takes no filter-spectra size: a buffer of another plan
+        # (another layer) would be read past its end on the device
+        p = _dev_tensor(wspec, "wspec")
+        if wspec.numel() * wspec.element_size() < self.info.wspec_bytes:
+            raise ValueError(f"wspec has {wspec.numel() * wspec.element_size()} bytes, the plan needs "
+                             f"{self.info.wspec_bytes}")
+        return p
+
     def conv2d(self, x, wspec, bias=None, out=None, workspace=None):
         torch = _torch()
         xp = _dev_tensor(x, "x", torch.float32, self.n * self.cin * self.h * self.w)
@@ -235,7 +246,7 @@ class Plan:
         yp = _dev_tensor(out, "y", torch.float32, _prod(self.out_shape))
         ws = self.new_workspace() if workspace is None else workspace
         bp = None if bias is None else _dev_tensor(bias, "bias", torch.float32, self.cout)
-        _check(lib().fftsplit_conv2d(self._h, xp, _dev_tensor(wspec, "wspec"), bp, yp, _dev_tensor(ws, "workspace"),
+        _check(lib().fftsplit_conv2d(self._h, xp, self._wspec(wspec), bp, yp, _dev_tensor(ws, "workspace"),
                                      ws.numel() * ws.element_size(), _stream_handle(self.device)),
                "fftsplit_conv2d")
         return out
@@ -248,7 +259,7 @@ class Plan:
                "fftsplit_forward")
 
     def contract(self, wspec, workspace):
-        _check(lib().fftsplit_contract(self._h, _dev_tensor(wspec, "wspec"), _dev_tensor(workspace, "workspace"),
+        _check(lib().fftsplit_contract(self._h, self._wspec(wspec), _dev_tensor(workspace, "workspace"),
                                        workspace.numel() * workspace.element_size(), _stream_handle(self.device)),
                "fftsplit_contract")
 
@@ -282,6 +293,8 @@ class Plan:
         out = self.new_output() if out is None else out
         yp = _dev_tensor(out, "y", torch.float32, self.n * self.cout * self.h * self.w)
         bp = None if bias is None else _dev_tensor(bias, "bias", torch.float32, self.cout)
+        if wd.numel() * wd.element_size() < self.info.direct_wspec_bytes:
+            raise ValueError("direct weight buffer too small for this plan")
         _check(lib().fftsplit_direct_conv2d(self._h, xp, _dev_tensor(wd, "wd"), bp, yp,
                                             _stream_handle(self.device)), "fftsplit_direct_conv2d")
         return out

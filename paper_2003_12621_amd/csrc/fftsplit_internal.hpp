@@ -44,6 +44,8 @@ struct fftsplit_plan_s {
     // band inverse):
     // conv2d sums the channels inside the inverse and skips the contraction
     bool fuse_cin;
+    // the cost model's terms for the chosen L (fftsplit_plan_info_t)
+    double model_con_flops, model_xfer_bytes, model_seconds;
 };
 
 namespace fftsplit {
@@ -128,6 +130,9 @@ hipError_t launch_forward(const fftsplit_plan_s& p, const float* x, float2* xspe
                           const LaunchEvents& ev);
 hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xspec, const float2* wspec, float2* yspec,
                            hipStream_t s, const LaunchEvents& ev);
+// whether launch_contract has a kernel for tile bm x bn, stages of kc and
+// 3 or 4 real products per complex multiply-add
+bool contract_variant_exists(int bm, int bn, int kc, int products);
 hipError_t launch_inverse(const fftsplit_plan_s& p, const float2* yspec, const float* bias, float* y, void* aux,
                           hipStream_t s, const LaunchEvents& ev);
 hipError_t launch_maxpool(const float* x, float* y, int n, int c, int h, int w, hipStream_t s,

@@ -384,6 +384,18 @@ static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, 
                          p.prob.cin, p.coutp, p.ntp, nbco, nbt, p.bins, patch_group(p.L), packed_slots(p.L));
 }
 
+// The variants launch_contract dispatches (checked at plan time, so that a
+// plan never names a tile without a kernel).
+bool contract_variant_exists(int bm, int bn, int kc, int products) {
+    const int v = bm * 1000000 + bn * 1000 + kc;
+    if (bm <= 0 || bn <= 0 || kc <= 0) return false;
+    if (products == 3) return v == 64064016 || v == 128064016 || v == 64128016 || v == 128032016;
+    if (products == 4)
+        return v == 64064016 || v == 64064032 || v == 128064016 || v == 128064032 || v == 64128016 ||
+               v == 128128016 || v == 256064016 || v == 128032016;
+    return false;
+}
+
 hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xs, const float2* ws, float2* ys,
                            hipStream_t s, const LaunchEvents& ev) {
     const int v = p.con_bm * 1000000 + p.con_bn * 1000 + p.con_kc;

@@ -45,7 +45,7 @@ static constexpr double kModelMatrixRate = 100.0e12;
 
 struct Geometry {
     int T, L, th, tw, nt, ntp, bins, coutp;
-    double model_seconds;
+    double con_flops, xfer_bytes, model_seconds;
 };
 
 static Geometry geometry(const fftsplit_problem_t& p, int L) {
@@ -68,6 +68,8 @@ static Geometry geometry(const fftsplit_problem_t& p, int L) {
     const double inv = 8.0 * F * coutp * ntp + 4.0 * img * p.cout;
     const double con = con_f / kModelMatrixRate > con_b / kModelBandwidth ? con_f / kModelMatrixRate
                                                                           : con_b / kModelBandwidth;
+    g.con_flops = con_f;
+    g.xfer_bytes = fwd + inv;
     g.model_seconds = fwd / kModelBandwidth + con + inv / kModelBandwidth;
     return g;
 }
@@ -269,6 +271,9 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     plan->ntp = g.ntp;
     plan->bins = g.bins;
     plan->coutp = g.coutp;
+    plan->model_con_flops = g.con_flops;
+    plan->model_xfer_bytes = g.xfer_bytes;
+    plan->model_seconds = g.model_seconds;
     plan->oaa = oaa;
     plan->bias = (p.flags & FFTSPLIT_BIAS) != 0;
     plan->relu = (p.flags & FFTSPLIT_RELU) != 0;
@@ -303,10 +308,15 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
             const char* q = v;
             if (!std::strncmp(q, "g3:", 3)) { prod = 3; q += 3; }
             else if (!std::strncmp(q, "g4:", 3)) { q += 3; }
-            int bm = 0, bn = 0, kc = 0;
-            if (std::sscanf(q, "%dx%dx%d", &bm, &bn, &kc) != 3) {
+            int bm = 0, bn = 0, kc = 0, used = 0;
+            if (std::sscanf(q, "%dx%dx%d%n", &bm, &bn, &kc, &used) != 3 || q[used] != '\0') {
                 delete plan;
                 return fail(FFTSPLIT_ERROR_INVALID_VALUE, "FFTSPLIT_CONTRACT_TILE must look like [g3:]BMxBNxKC");
+            }
+            if (!contract_variant_exists(bm, bn, kc, prod)) {
+                delete plan;
+                return fail(FFTSPLIT_ERROR_INVALID_VALUE, std::string("FFTSPLIT_CONTRACT_TILE=") + v +
+                                                              " names no contraction kernel variant");
             }
             plan->con_bm = bm;
             plan->con_bn = bn;
@@ -412,6 +422,9 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_plan_info(fftsplit_plan_t plan, fftsp
     i.spec_group = patch_group(plan->L);
     i.fused_channel_sum = plan->fuse_cin ? 1 : 0;
     i.contract_prefetch = plan->con_prefetch;
+    i.model_contract_flops = plan->model_con_flops;
+    i.model_transform_bytes = plan->model_xfer_bytes;
+    i.model_seconds = plan->model_seconds;
     *out = i;
     return FFTSPLIT_SUCCESS;
 }

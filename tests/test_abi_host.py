@@ -274,7 +274,7 @@ def test_contraction_prefetch_choice(monkeypatch):
     assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.contract_prefetch == 1
     monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", "g3:128x64x16")
     assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.contract_prefetch == 2
-    monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", "g3:64x64x32")
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", "g4:64x64x32")
     assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.contract_prefetch == 1
     monkeypatch.delenv("FFTSPLIT_CONTRACT_TILE")
     monkeypatch.setenv("FFTSPLIT_CONTRACT_PREFETCH", "1")
@@ -282,3 +282,14 @@ def test_contraction_prefetch_choice(monkeypatch):
     monkeypatch.setenv("FFTSPLIT_CONTRACT_PREFETCH", "3")
     assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.contract_prefetch == 3
     assert plan(n=32, cin=512, h=14, w=14, cout=512, k=3, tile=14).info.contract_prefetch == 2
+
+
+@pytest.mark.parametrize("value", ["0x0x0", "-64x64x16", "g3:64x64x32", "g3:256x64x16", "64x64x16junk",
+                                   "64x64", "g5:64x64x16", "96x64x16"])
+def test_contraction_tile_override_is_validated(value, monkeypatch):
+    """FFTSPLIT_CONTRACT_TILE is checked at plan time against the kernel
+    variants the contraction has: anything else is INVALID_VALUE, so that a
+    later conv2d cannot fail after its forward stage has been enqueued."""
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", value)
+    assert status_of(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28) == fs.ERROR_INVALID_VALUE
+    assert "FFTSPLIT_CONTRACT_TILE" in fs.last_error()

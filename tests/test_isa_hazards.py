@@ -36,8 +36,9 @@ def _regs_written(line):
 
 def _disassemble(obj, tmp):
     fb, co = os.path.join(tmp, "fb.bin"), os.path.join(tmp, "co.o")
-    subprocess.run([f"{LLVM}/llvm-objcopy", f"--dump-section=.hip_fatbin={fb}", obj], check=True,
-                   capture_output=True)
+    # (an explicit output file: without one, llvm-objcopy rewrites its input)
+    subprocess.run([f"{LLVM}/llvm-objcopy", f"--dump-section=.hip_fatbin={fb}", obj,
+                    os.path.join(tmp, "copy.o")], check=True, capture_output=True)
     subprocess.run([f"{LLVM}/clang-offload-bundler", "--unbundle", "--type=o",
                     "--targets=hipv4-amdgcn-amd-amdhsa--gfx950", f"--input={fb}", f"--output={co}"],
                    check=True, capture_output=True)
@@ -74,7 +75,10 @@ def test_scanner_finds_the_pattern():
 def test_built_code_has_no_store_data_hazard():
     objs = sorted(os.path.join(BUILD, f) for f in os.listdir(BUILD) if f.startswith("k_") and f.endswith(".o"))
     assert objs, "no kernel objects"
+    before = {o: os.stat(o).st_mtime_ns for o in objs}
     with tempfile.TemporaryDirectory() as tmp:
         for obj in objs:
             found = hazards(_disassemble(obj, tmp))
             assert not found, f"{os.path.basename(obj)}: {found[:3]}"
+    # the scan reads the build; it must not rewrite it
+    assert {o: os.stat(o).st_mtime_ns for o in objs} == before
