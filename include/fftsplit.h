@@ -219,6 +219,24 @@ fftsplit_status_t fftsplit_conv2d(fftsplit_plan_t plan, const float* x, const vo
                                   const float* bias, float* y, void* workspace,
                                   size_t workspace_bytes, hipStream_t stream);
 
+/* Bytes of the static device scratch behind fftsplit_conv2d_noalloc. */
+#define FFTSPLIT_NOALLOC_MAX_WORKSPACE (256u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * fftsplit_conv2d with the workspace taken from a static device array of
+ * FFTSPLIT_NOALLOC_MAX_WORKSPACE bytes (256 MiB) that the library holds on
+ * each device it runs on until the process ends.  Same arguments, layouts,
+ * kernels and results as fftsplit_conv2d, minus the workspace; calls no
+ * allocating routine.  Plans whose info.workspace_bytes exceed the limit
+ * get FFTSPLIT_ERROR_INSUFFICIENT_WORKSPACE (nothing enqueued).  Every call
+ * on a device shares that device's array: calls that overlap on one device
+ * (concurrent streams, or threads) race and must be serialised by the
+ * caller.  The array needs no clearing between calls.  The first call on a
+ * device looks up the array's device address (hipGetSymbolAddress). */
+fftsplit_status_t fftsplit_conv2d_noalloc(fftsplit_plan_t plan, const float* x, const void* wspec,
+                                          const float* bias, float* y, hipStream_t stream);
+
 /* The three stages of fftsplit_conv2d, separately (same arguments and
  * workspace layout; running them in order is exactly fftsplit_conv2d).
  * They exist for stage-by-stage testing and per-kernel timing.

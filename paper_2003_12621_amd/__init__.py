@@ -36,6 +36,10 @@ BIAS = 2
 RELU = 4
 MAXPOOL = 8
 
+# FFTSPLIT_NOALLOC_MAX_WORKSPACE of fftsplit.h: bytes of the static scratch
+# behind fftsplit_conv2d_noalloc
+NOALLOC_MAX_WORKSPACE = 256 << 20
+
 
 class Problem(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int), ("cin", ctypes.c_int), ("h", ctypes.c_int), ("w", ctypes.c_int),
@@ -78,6 +82,8 @@ _SIGNATURES = {
                                                   ctypes.c_void_p]),
     "fftsplit_conv2d": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "fftsplit_conv2d_noalloc": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                               ctypes.c_void_p, ctypes.c_void_p]),
     "fftsplit_forward": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                         ctypes.c_void_p]),
     "fftsplit_contract": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
@@ -249,6 +255,21 @@ class Plan:
         _check(lib().fftsplit_conv2d(self._h, xp, self._wspec(wspec), bp, yp, _dev_tensor(ws, "workspace"),
                                      ws.numel() * ws.element_size(), _stream_handle(self.device)),
                "fftsplit_conv2d")
+        return out
+
+    def conv2d_noalloc(self, x, wspec, bias=None, out=None):
+        """conv2d with the library's static device scratch as the workspace
+        (fftsplit_conv2d_noalloc): the library allocates nothing.  Needs
+        info.workspace_bytes <= NOALLOC_MAX_WORKSPACE; calls overlapping on
+        one device race on the shared scratch."""
+        torch = _torch()
+        xp = _dev_tensor(x, "x", torch.float32, self.n * self.cin * self.h * self.w)
+        if out is None:
+            raise ValueError("conv2d_noalloc needs a caller-allocated output (out=)")
+        yp = _dev_tensor(out, "y", torch.float32, _prod(self.out_shape))
+        bp = None if bias is None else _dev_tensor(bias, "bias", torch.float32, self.cout)
+        _check(lib().fftsplit_conv2d_noalloc(self._h, xp, self._wspec(wspec), bp, yp, _stream_handle(self.device)),
+               "fftsplit_conv2d_noalloc")
         return out
 
     def forward(self, x, workspace):

@@ -20,24 +20,6 @@ bool overlap(const void* a, size_t an, const void* b, size_t bn) {
     return a0 < b0 + bn && b0 < a0 + an;
 }
 
-// Makes the plan's device current for the duration of a call.
-class DeviceGuard {
-  public:
-    explicit DeviceGuard(int dev) {
-        ok_ = hipGetDevice(&prev_) == hipSuccess;
-        if (ok_ && prev_ != dev) ok_ = hipSetDevice(dev) == hipSuccess;
-        changed_ = ok_ && prev_ != dev;
-    }
-    ~DeviceGuard() {
-        if (changed_) (void)hipSetDevice(prev_);
-    }
-    bool ok() const { return ok_; }
-
-  private:
-    int prev_ = 0;
-    bool ok_ = false, changed_ = false;
-};
-
 fftsplit_status_t check_plan(fftsplit_plan_t plan) {
     if (!plan) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "plan is NULL");
     if (plan->device < 0)
@@ -162,23 +144,22 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_inverse(fftsplit_plan_t plan, const f
                     "inverse patch transform launch");
 }
 
-FFTSPLIT_EXPORT fftsplit_status_t fftsplit_conv2d(fftsplit_plan_t plan, const float* x, const void* wspec,
-                                                  const float* bias, float* y, void* workspace,
-                                                  size_t workspace_bytes, hipStream_t stream) {
-    set_error("");
+namespace fftsplit {
+
+fftsplit_status_t check_conv2d_args(fftsplit_plan_t plan, const float* x, const void* wspec, const float* bias,
+                                    const float* y) {
     if (fftsplit_status_t s = check_plan(plan)) return s;
     if (fftsplit_status_t s = check_ptr(x, "x")) return s;
     if (fftsplit_status_t s = check_ptr(wspec, "wspec")) return s;
     if (fftsplit_status_t s = check_ptr(y, "y")) return s;
     if (fftsplit_status_t s = check_bias(plan, bias)) return s;
-    if (fftsplit_status_t s = check_workspace(plan, workspace, workspace_bytes)) return s;
     if (overlap(x, x_bytes(plan), y, y_bytes(plan))) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "y overlaps x");
-    if (overlap(x, x_bytes(plan), workspace, plan->ws_bytes) || overlap(y, y_bytes(plan), workspace, plan->ws_bytes) ||
-        overlap(wspec, plan->wspec_bytes, workspace, plan->ws_bytes) ||
-        overlap(wspec, plan->wspec_bytes, y, y_bytes(plan)))
-        return fail(FFTSPLIT_ERROR_INVALID_VALUE, "buffers overlap");
-    DeviceGuard g(plan->device);
-    if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
+    if (overlap(wspec, plan->wspec_bytes, y, y_bytes(plan))) return fail(FFTSPLIT_ERROR_INVALID_VALUE, "buffers overlap");
+    return FFTSPLIT_SUCCESS;
+}
+
+fftsplit_status_t enqueue_conv2d(fftsplit_plan_t plan, const float* x, const void* wspec, const float* bias, float* y,
+                                 void* workspace, hipStream_t stream) {
     float2* xs = reinterpret_cast<float2*>(ws_at(workspace, plan->xspec_off));
     float2* ys = reinterpret_cast<float2*>(ws_at(workspace, plan->yspec_off));
     LaunchEvents first, middle, last;
@@ -194,6 +175,22 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_conv2d(fftsplit_plan_t plan, const fl
                                        "contraction launch"))
         return s;
     return launched(launch_inverse_to_y(plan, ys, bias, y, workspace, stream, last), "inverse patch transform launch");
+}
+
+}  // namespace fftsplit
+
+FFTSPLIT_EXPORT fftsplit_status_t fftsplit_conv2d(fftsplit_plan_t plan, const float* x, const void* wspec,
+                                                  const float* bias, float* y, void* workspace,
+                                                  size_t workspace_bytes, hipStream_t stream) {
+    set_error("");
+    if (fftsplit_status_t s = check_conv2d_args(plan, x, wspec, bias, y)) return s;
+    if (fftsplit_status_t s = check_workspace(plan, workspace, workspace_bytes)) return s;
+    if (overlap(x, x_bytes(plan), workspace, plan->ws_bytes) || overlap(y, y_bytes(plan), workspace, plan->ws_bytes) ||
+        overlap(wspec, plan->wspec_bytes, workspace, plan->ws_bytes))
+        return fail(FFTSPLIT_ERROR_INVALID_VALUE, "buffers overlap");
+    DeviceGuard g(plan->device);
+    if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
+    return enqueue_conv2d(plan, x, wspec, bias, y, workspace, stream);
 }
 
 FFTSPLIT_EXPORT fftsplit_status_t fftsplit_maxpool2x2(const float* x, float* y, int n, int c, int h, int w,

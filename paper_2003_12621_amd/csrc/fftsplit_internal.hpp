@@ -121,6 +121,32 @@ __host__ __device__ constexpr int bin_real_b(int L) { return L * L / 2 - 1; }
 void set_error(const std::string& msg);
 fftsplit_status_t fail(fftsplit_status_t st, const std::string& msg);
 
+// Makes the plan's device current for the duration of a call.
+class DeviceGuard {
+  public:
+    explicit DeviceGuard(int dev) {
+        ok_ = hipGetDevice(&prev_) == hipSuccess;
+        if (ok_ && prev_ != dev) ok_ = hipSetDevice(dev) == hipSuccess;
+        changed_ = ok_ && prev_ != dev;
+    }
+    ~DeviceGuard() {
+        if (changed_) (void)hipSetDevice(prev_);
+    }
+    bool ok() const { return ok_; }
+
+  private:
+    int prev_ = 0;
+    bool ok_ = false, changed_ = false;
+};
+
+// fftsplit_conv2d in two parts (api.cpp): the checks of every argument but
+// the workspace, and the launch sequence into a workspace of at least
+// plan->ws_bytes bytes on the plan's device, which must be current.
+fftsplit_status_t check_conv2d_args(fftsplit_plan_t plan, const float* x, const void* wspec, const float* bias,
+                                    const float* y);
+fftsplit_status_t enqueue_conv2d(fftsplit_plan_t plan, const float* x, const void* wspec, const float* bias, float* y,
+                                 void* workspace, hipStream_t stream);
+
 // Kernel launchers (one per .hip file); return hipSuccess or the launch
 // error.  `ev` optionally times the launch sequence (see launch_util.hpp).
 struct LaunchEvents;
