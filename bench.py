@@ -277,6 +277,49 @@ def _avg(v):
     return sum(v) / len(v)
 
 
+def hbm_floor(dev, mixes, steps=20):
+    """The streaming rates this GPU reaches, measured with plain torch
+    kernels, warm and cold (a 1 GiB read first): writing N bytes (fill_)
+    and copying N bytes (copy_, which reads and writes them).  On MI355X
+    reads and writes do not overlap, so reading costs the copy's time minus
+    the write's, and the floor of a kernel that reads R and writes W bytes
+    is R / read rate + W / write rate.  `mixes`: {name: (R, W)}."""
+    import torch
+    nbytes = 128 << 20
+    buf = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(buf)
+    flush = torch.ones(256 << 20, dtype=torch.float32, device=dev)   # 1 GiB
+
+    def timed(fn, cold):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        fn()
+        _sync()
+        for a, b in ev:
+            if cold:
+                flush.sum()
+            a.record()
+            fn()
+            b.record()
+        _sync()
+        ts = sorted(a.elapsed_time(b) for a, b in ev)
+        return ts[len(ts) // 2] * 1e-3   # median, seconds
+
+    out = {}
+    for cold in (False, True):
+        tag = "cold" if cold else "warm"
+        t_write = timed(lambda: dst.fill_(2.0), cold)
+        t_copy = timed(lambda: dst.copy_(buf), cold)
+        t_read = max(t_copy - t_write, 1e-9)
+        out[tag] = {"write_GB/s": round(nbytes / t_write / 1e9, 1), "copy_GB/s": round(2 * nbytes / t_copy / 1e9, 1),
+                    "read_GB/s": round(nbytes / t_read / 1e9, 1)}
+        for name, (r, w) in mixes.items():
+            out[tag][f"{name}_floor_us"] = round((r * t_read + w * t_write) / nbytes * 1e6, 2)
+    del buf, dst, flush
+    out["note"] = ("128 MiB buffers, medians of 20; write rate from fill_, read rate from copy_ minus fill_; "
+                   "floor of a kernel reading R and writing W bytes = R / read rate + W / write rate")
+    return out
+
+
 def stage_record(counts, fwd, con, inv):
     fwd_gbs = counts["forward_bytes"] / (fwd * 1e-3) / 1e9
     inv_gbs = counts["inverse_bytes"] / (inv * 1e-3) / 1e9
@@ -507,6 +550,8 @@ def main():
     ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache stage timings")
     ap.add_argument("--no-compare", action="store_true",
                     help="skip timing the spatial methods (this library's direct kernel, torch/MIOpen conv2d)")
+    ap.add_argument("--no-floor", action="store_true",
+                    help="skip measuring the streaming read/write rates (the transforms' practical floor)")
     ap.add_argument("--no-others", action="store_true",
                     help="skip the other workloads (the other single layers and the VGG-16 stack)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
@@ -623,6 +668,17 @@ def main():
         "wall_s_timed": round(t_wall, 4),
         "parity_rel_l2": parity,
     }
+    if not args.no_floor:
+        floor = hbm_floor(dev, {"forward": (4 * layer.n * layer.cin * layer.h * layer.w,
+                                            counts["forward_bytes"] - 4 * layer.n * layer.cin * layer.h * layer.w),
+                                "inverse": (counts["inverse_bytes"] - 4 * layer.n * layer.cout * layer.h * layer.w,
+                                            4 * layer.n * layer.cout * layer.h * layer.w)})
+        for st, name in (("forward", "forward"), ("inverse", "inverse")):
+            stages[st]["frac_of_floor_warm"] = round(floor["warm"][f"{name}_floor_us"] / (stages[st]["ms"] * 1e3), 4)
+            if out["stages_cold"] is not None:
+                out["stages_cold"][st]["frac_of_floor_cold"] = round(
+                    floor["cold"][f"{name}_floor_us"] / (out["stages_cold"][st]["ms"] * 1e3), 4)
+        out["hbm_floor"] = floor
     if not args.no_compare:
         out["spatial_methods"] = time_spatial_methods(steps, run)
         out["oaaconv"] = time_oaaconv(steps, layer, run.xd, run.wd, run.bd)

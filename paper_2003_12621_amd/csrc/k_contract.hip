@@ -30,10 +30,11 @@
 // multiplied out of LDS, then written to the other LDS buffer.  Inside a
 // stage the operand fragments of the next channel pair are read from LDS
 // while the current pair's MFMAs run.  The filter spectra, the bulk of the
-// bytes and each read once, are loaded non-temporally so they do not evict
-// the patch and output spectra.  The channel blocks of one bin are
-// consecutive logical workgroups on the same XCD, so the bin's patch
-// spectra are fetched from HBM once and reused from L2.
+// bytes, are loaded non-temporally where each block of them is read by one
+// workgroup, so they do not evict the patch and output spectra.  The
+// channel blocks of one bin are consecutive logical workgroups on the same
+// XCD, so the bin's patch spectra are fetched from HBM once and reused from
+// L2.
 #include "fftsplit_internal.hpp"
 #include "launch_util.hpp"
 
@@ -206,6 +207,11 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     const int t0 = tbk * BN;
 
     const float4* wsrc = reinterpret_cast<const float4*>(ws + size_t(f) * cin * coutp + co0);
+    // The filter spectra are streamed (non-temporal) when each block of them
+    // is read by one workgroup only (one patch block per bin); with several
+    // patch blocks per bin every workgroup of the bin reads the same block,
+    // which then has to stay in the caches.
+    const bool w_once = nbt == 1;
     const int wrow4 = coutp / 2;   // row pitch in float4
     // Patch spectra are channel-blocked (fftsplit.h): input channel ci of
     // bin f starts at spec_offset(ci, f, 0); within a block of 16 channels
@@ -229,8 +235,8 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
         for (int i = 0; i < S::WL; ++i) {
             const int e = i * S::NT + tid;
             const int ci = k0 + e / (BM / 2);
-            wreg[i] = load_stream_u4(reinterpret_cast<const uint4*>(wsrc) + (full ? ci : min(ci, cin - 1)) * wrow4 +
-                                     e % (BM / 2));
+            const uint4* g = reinterpret_cast<const uint4*>(wsrc) + (full ? ci : min(ci, cin - 1)) * wrow4 + e % (BM / 2);
+            wreg[i] = w_once ? load_stream_u4(g) : *g;
         }
 #pragma unroll
         for (int i = 0; i < S::XL; ++i) {
@@ -322,7 +328,8 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
             for (int i = 0; i < S::WL; ++i) {
                 const int e = i * S::NT + tid;
                 const uint4* g = reinterpret_cast<const uint4*>(wsrc) + (k0 + e / (BM / 2)) * wrow4 + e % (BM / 2);
-                lds_dma16<true>(g, sw + i * S::NT + wbase);   // non-temporal, as load_stream_u4
+                if (w_once) lds_dma16<true>(g, sw + i * S::NT + wbase);   // non-temporal, as load_stream_u4
+                else lds_dma16<false>(g, sw + i * S::NT + wbase);
             }
 #pragma unroll
             for (int i = 0; i < S::XL; ++i) {
