@@ -278,46 +278,75 @@ def _avg(v):
 
 
 def hbm_floor(dev, mixes, steps=20):
-    """The streaming rates this GPU reaches, measured with plain torch
-    kernels, warm and cold (a 1 GiB read first): writing N bytes (fill_)
-    and copying N bytes (copy_, which reads and writes them).  On MI355X
-    reads and writes do not overlap, so reading costs the copy's time minus
-    the write's, and the floor of a kernel that reads R and writes W bytes
-    is R / read rate + W / write rate.  `mixes`: {name: (R, W)}."""
+    """What HBM sustains for each transform's byte mix on this GPU: the
+    library's streaming probe (fftsplit_probe_stream: a plain kernel that
+    reads R and writes W bytes from 8192 workgroups) timed warm (its input
+    just read by the previous run) and cold (after a 512 MB read has
+    replaced the last-level cache's contents), median of `steps` launches.
+    `mixes`: {name: (R, W)}."""
     import torch
-    nbytes = 128 << 20
-    buf = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
-    dst = torch.empty_like(buf)
-    flush = torch.ones(256 << 20, dtype=torch.float32, device=dev)   # 1 GiB
+    import paper_2003_12621_amd as fs
+    r16 = lambda b: (int(b) + 15) // 16 * 16  # noqa: E731
+    big = max(max(r16(r), r16(w)) for r, w in mixes.values())
+    src = torch.ones(big // 4 + 64, dtype=torch.float32, device=dev)
+    dst = torch.empty(big // 4 + 64, dtype=torch.float32, device=dev)
+    flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)   # 512 MB
 
-    def timed(fn, cold):
+    def timed(r, w, cold):
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-        fn()
+        fs.probe_stream(src, dst, r, w)
         _sync()
         for a, b in ev:
             if cold:
                 flush.sum()
             a.record()
-            fn()
+            fs.probe_stream(src, dst, r, w)
             b.record()
         _sync()
         ts = sorted(a.elapsed_time(b) for a, b in ev)
-        return ts[len(ts) // 2] * 1e-3   # median, seconds
+        return ts[len(ts) // 2] * 1e3   # median, us
 
     out = {}
     for cold in (False, True):
         tag = "cold" if cold else "warm"
-        t_write = timed(lambda: dst.fill_(2.0), cold)
-        t_copy = timed(lambda: dst.copy_(buf), cold)
-        t_read = max(t_copy - t_write, 1e-9)
-        out[tag] = {"write_GB/s": round(nbytes / t_write / 1e9, 1), "copy_GB/s": round(2 * nbytes / t_copy / 1e9, 1),
-                    "read_GB/s": round(nbytes / t_read / 1e9, 1)}
+        out[tag] = {}
         for name, (r, w) in mixes.items():
-            out[tag][f"{name}_floor_us"] = round((r * t_read + w * t_write) / nbytes * 1e6, 2)
-    del buf, dst, flush
-    out["note"] = ("128 MiB buffers, medians of 20; write rate from fill_, read rate from copy_ minus fill_; "
-                   "floor of a kernel reading R and writing W bytes = R / read rate + W / write rate")
+            t = timed(r16(r), r16(w), cold)
+            out[tag][f"{name}_floor_us"] = round(t, 2)
+            out[tag][f"{name}_floor_frac_hbm"] = round((r + w) / (t * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+    del src, dst, flush
+    out["note"] = ("fftsplit_probe_stream (plain streaming kernel, 8192 workgroups) moving each transform's read "
+                   "and write bytes; median of 20 launches; cold = after a 512 MB read")
     return out
+
+
+def matrix_ceiling(run, con_ms, steps=20):
+    """What the fp32 matrix cores sustain for the contraction's launch: the
+    library's matrix probe (fftsplit_probe_matrix: the same grid and
+    occupancy, the same matrix operations per wave, operands in registers,
+    no memory traffic), median of `steps` launches."""
+    import torch
+    plan, i = run.plan, run.info
+    sink = plan.probe_matrix()
+    for _ in range(3):
+        plan.probe_matrix(sink)
+    _sync()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in ev:
+        a.record()
+        plan.probe_matrix(sink)
+        b.record()
+    _sync()
+    ts = sorted(a.elapsed_time(b) for a, b in ev)
+    probe_us = ts[len(ts) // 2] * 1e3
+    kc = i.contract_stage_k
+    executed = 2 * i.contract_real_products * i.bins * i.cout_padded * i.tiles_padded * (-(-run.layer.cin // kc) * kc)
+    return {"probe_us": round(probe_us, 2), "contract_us": round(con_ms * 1e3, 2),
+            "executed_flops": executed,
+            "probe_frac_of_peak": round(executed / (probe_us * 1e-6) / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4),
+            "contract_vs_probe": round(probe_us / (con_ms * 1e3), 4),
+            "note": "fftsplit_probe_matrix: the contraction's grid, occupancy and matrix operations per wave with "
+                    "no memory traffic; contract_vs_probe = probe time / contraction time (warm)"}
 
 
 def stage_record(counts, fwd, con, inv):
@@ -551,7 +580,8 @@ def main():
     ap.add_argument("--no-compare", action="store_true",
                     help="skip timing the spatial methods (this library's direct kernel, torch/MIOpen conv2d)")
     ap.add_argument("--no-floor", action="store_true",
-                    help="skip measuring the streaming read/write rates (the transforms' practical floor)")
+                    help="skip the practical ceilings: the streaming probe of the transforms' byte mixes and "
+                         "the matrix probe of the contraction's launch")
     ap.add_argument("--no-others", action="store_true",
                     help="skip the other workloads (the other single layers and the VGG-16 stack)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
@@ -679,6 +709,8 @@ def main():
                 out["stages_cold"][st]["frac_of_floor_cold"] = round(
                     floor["cold"][f"{name}_floor_us"] / (out["stages_cold"][st]["ms"] * 1e3), 4)
         out["hbm_floor"] = floor
+    if not args.no_floor and not info.fused_channel_sum:
+        out["matrix_ceiling"] = matrix_ceiling(run, _avg(con))
     if not args.no_compare:
         out["spatial_methods"] = time_spatial_methods(steps, run)
         out["oaaconv"] = time_oaaconv(steps, layer, run.xd, run.wd, run.bd)

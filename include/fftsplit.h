@@ -285,6 +285,35 @@ fftsplit_status_t fftsplit_maxpool2x2(const float* x, float* y, int n, int c, in
  * device.  Always returns FFTSPLIT_SUCCESS. */
 fftsplit_status_t fftsplit_set_timing_events(hipEvent_t start, hipEvent_t stop);
 
+/* Measurement hooks: the practical ceilings the path's kernels are
+ * measured against, on the device they run on.  Neither computes anything
+ * of the method.
+ *
+ * fftsplit_probe_matrix: enqueues on `stream` (on the plan's device) one
+ * kernel with the plan's contraction launch -- the same grid of 256-thread
+ * workgroups and the same dynamic LDS, hence the same workgroups per
+ * compute unit -- in which every wave issues as many fp32 matrix
+ * operations (v_mfma_f32_32x32x2f32) as a wave of fftsplit_contract does,
+ * with operands in registers and no other memory traffic.  Its duration is
+ * the time the matrix cores need for the contraction's executed
+ * operations at this launch shape.  `sink` (device, one float) is written
+ * only if the sum of a wave's accumulators is exactly -1, which it never
+ * is.  INVALID_VALUE for a NULL plan or sink or an architecture-only plan;
+ * NOT_SUPPORTED for a plan whose channel sum runs inside the inverse (it
+ * has no contraction).
+ *
+ * fftsplit_probe_stream: enqueues on `stream` (current device) a plain
+ * streaming kernel that loads `read_bytes` from src and stores
+ * `write_bytes` to dst, 16 bytes per lane, from 8192 workgroups of 256
+ * threads: dst[i] = src[i] for the first min(read_bytes, write_bytes)
+ * bytes, zero for the rest of dst.  Its duration is what HBM needs for
+ * that read/write mix (e.g. a transform's bytes).  Both pointers device,
+ * 16-byte aligned, sizes multiples of 16, not overlapping; INVALID_VALUE
+ * otherwise. */
+fftsplit_status_t fftsplit_probe_matrix(fftsplit_plan_t plan, float* sink, hipStream_t stream);
+fftsplit_status_t fftsplit_probe_stream(const void* src, void* dst, size_t read_bytes, size_t write_bytes,
+                                        hipStream_t stream);
+
 /* Static description of a status code. */
 const char* fftsplit_status_string(fftsplit_status_t status);
 

@@ -97,6 +97,9 @@ _SIGNATURES = {
     "fftsplit_direct_conv2d": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                               ctypes.c_void_p, ctypes.c_void_p]),
     "fftsplit_set_timing_events": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
+    "fftsplit_probe_matrix": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+    "fftsplit_probe_stream": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_size_t,
+                                             ctypes.c_void_p]),
     "fftsplit_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "fftsplit_last_error": (ctypes.c_char_p, []),
 }
@@ -320,6 +323,21 @@ class Plan:
                                             _stream_handle(self.device)), "fftsplit_direct_conv2d")
         return out
 
+    # -- measurement hook ---------------------------------------------------
+    def probe_matrix(self, sink=None):
+        """Enqueue the matrix-core probe of this plan's contraction launch
+        (fftsplit_probe_matrix): same grid and occupancy, the same fp32
+        matrix operations per wave, no memory traffic.  `sink`: a CUDA
+        float32 tensor of at least one element (allocated if None)."""
+        torch = _torch()
+        if sink is None:
+            sink = torch.zeros(1, dtype=torch.float32, device=self.device)
+        if sink.numel() < 1:
+            raise ValueError("sink needs one element")
+        _check(lib().fftsplit_probe_matrix(self._h, _dev_tensor(sink, "sink", torch.float32),
+                                           _stream_handle(self.device)), "fftsplit_probe_matrix")
+        return sink
+
     # -- views of the workspace (complex64), for stage-level tests -------
     def _unblock(self, raw, channels):
         # channel-blocked [c/16][bins][c%16][tiles_padded] -> [bins][c][tiles_padded] (a copy)
@@ -360,6 +378,17 @@ def set_timing_events(start=None, stop=None):
             raise ValueError("event has no device handle yet; record it once first")
         return ctypes.c_void_p(h)
     _check(lib().fftsplit_set_timing_events(handle(start), handle(stop)), "fftsplit_set_timing_events")
+
+
+def probe_stream(src, dst, read_bytes, write_bytes):
+    """Enqueue the streaming probe (fftsplit_probe_stream): load
+    `read_bytes` of src and store `write_bytes` to dst (CUDA tensors, on
+    the current stream of their device)."""
+    for t, nb, name in ((src, read_bytes, "src"), (dst, write_bytes, "dst")):
+        if nb > t.numel() * t.element_size():
+            raise ValueError(f"{name} holds fewer than {nb} bytes")
+    _check(lib().fftsplit_probe_stream(_dev_tensor(src, "src"), _dev_tensor(dst, "dst"), int(read_bytes),
+                                       int(write_bytes), _stream_handle(dst.device)), "fftsplit_probe_stream")
 
 
 def maxpool2x2(x, out=None):

@@ -17,7 +17,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libfftsplit.so")
 
 SOURCES = ["plan.cpp", "api.cpp", "k_weights.hip", "k_forward.hip", "k_contract.hip", "k_inverse.hip", "k_pool.hip",
-           "k_direct.hip", "k_oaa.hip", "noalloc.hip"]
+           "k_direct.hip", "k_oaa.hip", "noalloc.hip", "k_probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

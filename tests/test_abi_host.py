@@ -134,6 +134,7 @@ def test_arch_only_plan_cannot_launch():
     assert L.fftsplit_forward(p._h, fake, fake, 1 << 30, None) == fs.ERROR_INVALID_VALUE
     assert L.fftsplit_direct_conv2d(p._h, fake, fake, None, fake, None) == fs.ERROR_INVALID_VALUE
     assert L.fftsplit_direct_transform_weights(p._h, fake, fake, None) == fs.ERROR_INVALID_VALUE
+    assert L.fftsplit_probe_matrix(p._h, fake, None) == fs.ERROR_INVALID_VALUE
 
 
 def test_auto_tile_choice_and_env_override(monkeypatch):
@@ -293,3 +294,16 @@ def test_contraction_tile_override_is_validated(value, monkeypatch):
     monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", value)
     assert status_of(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28) == fs.ERROR_INVALID_VALUE
     assert "FFTSPLIT_CONTRACT_TILE" in fs.last_error()
+
+
+def test_probe_argument_checks():
+    """The measurement hooks reject bad arguments before touching a device."""
+    L = fs.lib()
+    a, b = ctypes.c_void_p(1 << 20), ctypes.c_void_p(1 << 24)
+    assert L.fftsplit_probe_matrix(None, a, None) == fs.ERROR_INVALID_VALUE
+    assert L.fftsplit_probe_matrix(plan()._h, None, None) == fs.ERROR_INVALID_VALUE
+    assert L.fftsplit_probe_stream(None, b, 16, 16, None) == fs.ERROR_INVALID_VALUE         # NULL source
+    assert L.fftsplit_probe_stream(a, b, 24, 16, None) == fs.ERROR_INVALID_VALUE            # size not x16
+    assert L.fftsplit_probe_stream(ctypes.c_void_p((1 << 20) + 8), b, 16, 16, None) == fs.ERROR_INVALID_VALUE
+    assert L.fftsplit_probe_stream(a, ctypes.c_void_p((1 << 20) + 16), 64, 64, None) == fs.ERROR_INVALID_VALUE  # overlap
+    assert L.fftsplit_probe_stream(None, None, 0, 0, None) == fs.SUCCESS                  # nothing to do
