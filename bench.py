@@ -277,12 +277,26 @@ def _avg(v):
     return sum(v) / len(v)
 
 
+def dispatch_events(n):
+    """n (start, stop) pairs of timing events for fftsplit_set_timing_events
+    (each recorded once so that it has a device handle), the way the stage
+    times are taken: from the kernels' own dispatch timestamps."""
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for a, b in ev:
+        a.record()
+        b.record()
+    _sync()
+    return ev
+
+
 def hbm_floor(dev, mixes, steps=20):
     """What HBM sustains for each transform's byte mix on this GPU: the
     library's streaming probe (fftsplit_probe_stream: a plain kernel that
-    reads R and writes W bytes from 8192 workgroups) timed warm (its input
-    just read by the previous run) and cold (after a 512 MB read has
-    replaced the last-level cache's contents), median of `steps` launches.
+    reads R and writes W bytes from 8192 workgroups) timed like the stages
+    (dispatch timestamps), warm (its input just read by the previous run)
+    and cold (after a 512 MB read has replaced the last-level cache's
+    contents), median of `steps` launches.
     `mixes`: {name: (R, W)}."""
     import torch
     import paper_2003_12621_amd as fs
@@ -293,15 +307,15 @@ def hbm_floor(dev, mixes, steps=20):
     flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)   # 512 MB
 
     def timed(r, w, cold):
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        ev = dispatch_events(steps)
         fs.probe_stream(src, dst, r, w)
         _sync()
         for a, b in ev:
             if cold:
                 flush.sum()
-            a.record()
+            fs.set_timing_events(a, b)
             fs.probe_stream(src, dst, r, w)
-            b.record()
+            fs.set_timing_events()
         _sync()
         ts = sorted(a.elapsed_time(b) for a, b in ev)
         return ts[len(ts) // 2] * 1e3   # median, us
@@ -314,9 +328,12 @@ def hbm_floor(dev, mixes, steps=20):
             t = timed(r16(r), r16(w), cold)
             out[tag][f"{name}_floor_us"] = round(t, 2)
             out[tag][f"{name}_floor_frac_hbm"] = round((r + w) / (t * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+    # the same kernel moving 16 bytes: the fixed cost of one launch, timed this way
+    out["launch_us"] = round(timed(16, 16, False), 2)
     del src, dst, flush
     out["note"] = ("fftsplit_probe_stream (plain streaming kernel, 8192 workgroups) moving each transform's read "
-                   "and write bytes; median of 20 launches; cold = after a 512 MB read")
+                   "and write bytes, timed from its dispatch timestamps like the stages; median of 20 launches; "
+                   "cold = after a 512 MB read; launch_us: the same kernel moving 16 bytes")
     return out
 
 
@@ -324,18 +341,18 @@ def matrix_ceiling(run, con_ms, steps=20):
     """What the fp32 matrix cores sustain for the contraction's launch: the
     library's matrix probe (fftsplit_probe_matrix: the same grid and
     occupancy, the same matrix operations per wave, operands in registers,
-    no memory traffic), median of `steps` launches."""
+    no memory traffic), timed like the stages, median of `steps` launches."""
     import torch
     plan, i = run.plan, run.info
     sink = plan.probe_matrix()
     for _ in range(3):
         plan.probe_matrix(sink)
     _sync()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    ev = dispatch_events(steps)
     for a, b in ev:
-        a.record()
+        run.fs.set_timing_events(a, b)
         plan.probe_matrix(sink)
-        b.record()
+        run.fs.set_timing_events()
     _sync()
     ts = sorted(a.elapsed_time(b) for a, b in ev)
     probe_us = ts[len(ts) // 2] * 1e3

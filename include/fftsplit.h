@@ -280,7 +280,8 @@ fftsplit_status_t fftsplit_maxpool2x2(const float* x, float* y, int n, int c, in
  * stage call made by this thread records `start` (if non-NULL) when its
  * first kernel begins executing and `stop` (if non-NULL) when its last
  * kernel ends, using the kernels' own dispatch timestamps
- * (hipExtLaunchKernel) rather than separate event packets.  The events
+ * (hipExtLaunchKernel) rather than separate event packets; the two
+ * measurement probes below are timed the same way.  The events
  * must be valid hipEvents created with timing enabled, on the plan's
  * device.  Always returns FFTSPLIT_SUCCESS. */
 fftsplit_status_t fftsplit_set_timing_events(hipEvent_t start, hipEvent_t stop);

@@ -236,6 +236,10 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_direct_conv2d(fftsplit_plan_t plan, c
     return launched(launch_direct(*plan, x, wd, bias, y, stream, t_events), "direct convolution launch");
 }
 
+namespace fftsplit {
+LaunchEvents timing_events() { return t_events; }
+}  // namespace fftsplit
+
 FFTSPLIT_EXPORT fftsplit_status_t fftsplit_set_timing_events(hipEvent_t start, hipEvent_t stop) {
     set_error("");
     t_events.start = start;

@@ -487,16 +487,16 @@ hipError_t launch_forward(const fftsplit_plan_s& p, const float* x, float2* xs, 
     if (p.L % 2) return launch_oaa_forward(p, x, xs, s, ev);
     if (p.fwd_band) {
         switch (p.L) {
-            case 8: return launch_forward_band<8, 64, kBandNV8>(p, x, xs, s, ev);
-            case 16: return launch_forward_band<16, 32, kBandNV16>(p, x, xs, s, ev);
-            case 32: return launch_forward_band<32, 16, kBandNV32>(p, x, xs, s, ev);
+            case 8: return launch_forward_band<8, forward_group(8), kBandNV8>(p, x, xs, s, ev);
+            case 16: return launch_forward_band<16, forward_group(16), kBandNV16>(p, x, xs, s, ev);
+            case 32: return launch_forward_band<32, forward_group(32), kBandNV32>(p, x, xs, s, ev);
         }
         return hipErrorInvalidValue;
     }
     switch (p.L) {
-        case 8: return launch_forward_L<8, 64>(p, x, xs, s, ev);
-        case 16: return launch_forward_L<16, 32>(p, x, xs, s, ev);
-        case 32: return launch_forward_L<32, 16>(p, x, xs, s, ev);
+        case 8: return launch_forward_L<8, forward_group(8)>(p, x, xs, s, ev);
+        case 16: return launch_forward_L<16, forward_group(16)>(p, x, xs, s, ev);
+        case 32: return launch_forward_L<32, forward_group(32)>(p, x, xs, s, ev);
     }
     return hipErrorInvalidValue;
 }

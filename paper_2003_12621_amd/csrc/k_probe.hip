@@ -85,17 +85,18 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_probe_matrix(fftsplit_plan_t plan, fl
     if (nb < 1 || nb > 0x7fffffffLL) return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "grid size out of range");
     DeviceGuard g(plan->device);
     if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");
+    const LaunchEvents ev = timing_events();
     hipError_t e;
     if (plan->con_products == 3) {
         e = allow_dynamic_lds(matrix_probe_kernel<3>, lds);
         if (e == hipSuccess)
-            e = launch_kernel(matrix_probe_kernel<3>, dim3(unsigned(nb)), dim3(256), unsigned(lds), stream, nullptr,
-                              nullptr, sink, int(per_wave / 3), 1.0f);
+            e = launch_kernel(matrix_probe_kernel<3>, dim3(unsigned(nb)), dim3(256), unsigned(lds), stream, ev.start,
+                              ev.stop, sink, int(per_wave / 3), 1.0f);
     } else {
         e = allow_dynamic_lds(matrix_probe_kernel<4>, lds);
         if (e == hipSuccess)
-            e = launch_kernel(matrix_probe_kernel<4>, dim3(unsigned(nb)), dim3(256), unsigned(lds), stream, nullptr,
-                              nullptr, sink, int(per_wave / 4), 1.0f);
+            e = launch_kernel(matrix_probe_kernel<4>, dim3(unsigned(nb)), dim3(256), unsigned(lds), stream, ev.start,
+                              ev.stop, sink, int(per_wave / 4), 1.0f);
     }
     if (e != hipSuccess) return fail(FFTSPLIT_ERROR_DEVICE, std::string("matrix probe launch: ") + hipGetErrorString(e));
     return FFTSPLIT_SUCCESS;
@@ -111,7 +112,8 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_probe_stream(const void* src, void* d
     if (read_bytes && write_bytes && probe_overlap(src, read_bytes, dst, write_bytes))
         return fail(FFTSPLIT_ERROR_INVALID_VALUE, "src and dst overlap");
     if (!read_bytes && !write_bytes) return FFTSPLIT_SUCCESS;
-    const hipError_t e = launch_kernel(stream_probe_kernel, dim3(8192), dim3(256), 0u, stream, nullptr, nullptr,
+    const LaunchEvents ev = timing_events();
+    const hipError_t e = launch_kernel(stream_probe_kernel, dim3(8192), dim3(256), 0u, stream, ev.start, ev.stop,
                                        static_cast<const float4*>(src), static_cast<float4*>(dst),
                                        (long long)(read_bytes / 16), (long long)(write_bytes / 16));
     if (e != hipSuccess) return fail(FFTSPLIT_ERROR_DEVICE, std::string("stream probe launch: ") + hipGetErrorString(e));

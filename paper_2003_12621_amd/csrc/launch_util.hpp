@@ -118,6 +118,9 @@ struct LaunchEvents {
     hipEvent_t stop = nullptr;
 };
 
+// The calling thread's timing events (fftsplit_set_timing_events).
+LaunchEvents timing_events();
+
 template <typename K, typename... Args>
 inline hipError_t launch_kernel(K kernel, dim3 grid, dim3 block, unsigned lds, hipStream_t s, hipEvent_t start,
                                 hipEvent_t stop, Args... args) {

@@ -131,7 +131,7 @@ static void choose_forward_band(fftsplit_plan_s& p) {
         return;
     if (const char* e = std::getenv("FFTSPLIT_FORWARD_BAND"))
         if (*e == '0') return;
-    const int tg = patch_group(L);
+    const int tg = forward_group(L);
     const int nw = tg * (L / 2) / 64;
     const int rpi = 64 / (w / 4);
     const int nv = L == 8 ? kBandNV8 : (L == 16 ? kBandNV16 : kBandNV32);
