@@ -75,6 +75,9 @@ EDGE = [
     ((32, 16, 14, 14, 128, 3), 14),  # one patch per image: patches padded to 32, 128x32 tiles
     ((3, 20, 28, 28, 256, 3), 14),   # 12 patches padded to 32
     ((5, 8, 40, 40, 130, 3), 30),    # output channels not in 128s: padded to 64
+    ((1, 5, 23, 300, 7, 3), 30),     # width beyond the row-band kernels' 256: general forward / inverse, L = 32
+    ((2, 4, 19, 264, 9, 5), 12),     # the same at L = 16, K = 5
+    ((1, 3, 9, 258, 4, 3), 6),       # the same at L = 8
 ]
 
 
