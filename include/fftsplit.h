@@ -168,12 +168,6 @@ typedef struct {
     double model_contract_flops;
     double model_transform_bytes;
     double model_seconds;
-    /* Patch blocks (contract_tile_n patches each) of one bin and output-
-     * channel block that one contraction workgroup runs in sequence, the
-     * first channel stages of the next block loaded while the current one
-     * finishes: the largest of 8, 4, 2 that divides the bin's blocks and
-     * leaves at least two workgroups per compute unit, else 1. */
-    int contract_tiles_per_group;
 } fftsplit_plan_info_t;
 
 /* Validate `prob` (host) and create a plan for `device` (a HIP ordinal).
@@ -187,8 +181,7 @@ typedef struct {
  * the environment variable FFTSPLIT_TILE forces a tile size.  No device memory is touched.  *out is set only on success.
  * Other environment variables read here (for experiments; the defaults are
  * the measured best): FFTSPLIT_CONTRACT_TILE (see contract_tile_m),
- * FFTSPLIT_CONTRACT_PREFETCH (see contract_prefetch), FFTSPLIT_CONTRACT_TPW
- * (see contract_tiles_per_group),
+ * FFTSPLIT_CONTRACT_PREFETCH (see contract_prefetch),
  * FFTSPLIT_FORWARD_BAND=0 / FFTSPLIT_INVERSE_BAND=0 (general forward /
  * inverse kernels instead of the row-band ones), FFTSPLIT_FUSE_CIN=0 (no
  * channel sum in the inverse), FFTSPLIT_LOG=1 (print the plan to stderr). */

@@ -26,8 +26,6 @@ struct fftsplit_plan_s {
     // 3 (Gauss) or 4 real products per complex multiply-add; con_prefetch
     // stages loaded ahead of the one being multiplied (1 to 3)
     int con_bm, con_bn, con_kc, con_products, con_prefetch;
-    // patch blocks of one bin and channel block per contraction workgroup
-    int con_tpw;
     // overlap-save band variant of the forward transform (band.hpp):
     // used if fwd_band; LDS row pitch, left zero columns, zero-row slot and
     // dynamic LDS bytes

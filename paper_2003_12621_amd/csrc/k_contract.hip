@@ -185,8 +185,7 @@ __device__ __forceinline__ void multiply_stage(const float2* stage, floatx16 (&a
 template <int BM, int BN, int KC, int WM, bool G3, int PF>
 __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict__ xs, const float2* __restrict__ ws,
                                                        float2* __restrict__ ys, int cin, int coutp, int ntp,
-                                                       int nbco, int nbt, int nbins, int ygroup, int npacked,
-                                                       int tpw) {
+                                                       int nbco, int nbt, int nbins, int ygroup, int npacked) {
     using S = ConShape<BM, BN, KC, WM>;
     constexpr int TM = S::TM, TN = S::TN;
     extern __shared__ float4 lds_raw[];   // max(PF + 1, 2) stage buffers
@@ -199,17 +198,13 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
     const int cbk = lb % nbco;
     const int rest = lb / nbco;
-    // tpw consecutive patch blocks of one bin and channel block per
-    // workgroup (tpw divides nbt; tpw > 1 only with cin a multiple of KC
-    // and stages loaded ahead through LDS)
-    const int nbtg = nbt / tpw;
-    const int tbk = (rest % nbtg) * tpw;
-    const int f = rest / nbtg;
+    const int tbk = rest % nbt;
+    const int f = rest / nbt;
     // the last two bins (even L) are slots of two real bins each
     // (fftsplit.h): their products are taken component by component
     const bool packed = f >= nbins - npacked;
     const int co0 = cbk * BM;
-    const int t0 = tbk * BN;   // the first patch block's first patch
+    const int t0 = tbk * BN;
 
     const float4* wsrc = reinterpret_cast<const float4*>(ws + size_t(f) * cin * coutp + co0);
     // The filter spectra are streamed (non-temporal) when each block of them
@@ -221,8 +216,8 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     // Patch spectra are channel-blocked (fftsplit.h): input channel ci of
     // bin f starts at spec_offset(ci, f, 0); within a block of 16 channels
     // the rows are ntp apart.
-    auto xrow = [&](int ci, int tb = 0) {
-        return reinterpret_cast<const float4*>(xs + spec_offset(ci, f, t0 + tb * BN, nbins, ntp));
+    auto xrow = [&](int ci) {
+        return reinterpret_cast<const float4*>(xs + spec_offset(ci, f, t0, nbins, ntp));
     };
 
     // register sets for the stages loaded ahead (the second only with PF 2)
@@ -280,19 +275,16 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     // 3M: accR = sum Wr Xr, accI = sum Wi Xi, acc3 = sum (Wr + Wi)(Xr + Xi);
     //     Y = (accR - accI, acc3 - accR - accI).
     floatx16 accR[TM][TN], accI[TM][TN], acc3[G3 ? TM : 1][G3 ? TN : 1];
-    auto zero_acc = [&]() {
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j)
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    accR[i][j][r] = 0.f;
-                    accI[i][j][r] = 0.f;
-                    if (G3) acc3[G3 ? i : 0][G3 ? j : 0][r] = 0.f;
-                }
-    };
-    zero_acc();
+            for (int r = 0; r < 16; ++r) {
+                accR[i][j][r] = 0.f;
+                accI[i][j][r] = 0.f;
+                if (G3) acc3[G3 ? i : 0][G3 ? j : 0][r] = 0.f;
+            }
 
     const int nstage = (cin + KC - 1) / KC;
     const int krow = lane >> 5;
@@ -300,11 +292,6 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     // the multiply of the stage held in LDS buffer `stage`
     auto multiply = [&](const float2* stage) {
         multiply_stage<BM, BN, KC, TM, TN, G3>(stage, accR, accI, acc3, krow, col, wm, wn, packed);
-    };
-    // the outputs of patch block tb (of this workgroup's tpw)
-    auto store_tile = [&](int tb) {
-        store_output_tile<TM, TN, G3>(ys, accR, accI, acc3, co0 + wm * (TM * 32), t0 + tb * BN + wn * (TN * 32), f,
-                                      nbins, ygroup, ntp, krow, col, packed);
     };
     if constexpr (PF == 1) {
         float2* lds = reinterpret_cast<float2*>(lds_raw);   // [2][WE + XE]
@@ -332,16 +319,8 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
         float2* const bufs[4] = {lds, lds + (S::WE + S::XE), lds + 2 * (S::WE + S::XE), lds + 3 * (S::WE + S::XE)};
         static_assert(NB <= 4, "at most four stage buffers");
         constexpr int LPS = S::WL + S::XL;   // memory instructions per stage and thread
-        const int nfull = cin / KC;          // stages [0, nfull) of a patch block are whole
-        // Stages run through the workgroup's patch blocks in order: stage sg
-        // is channel stage sg % nfull of patch block sg / nfull, so the
-        // first stages of the next block are loaded while the current one
-        // finishes, and a block's outputs are stored when its last stage is
-        // multiplied.
-        const int total = nfull * tpw;
-        auto dma_stage = [&](int sg, float2* stage) {
-            const int tb = sg / nfull;
-            const int k0 = (sg - tb * nfull) * KC;
+        const int nfull = cin / KC;          // stages [0, nfull) are whole
+        auto dma_stage = [&](int k0, float2* stage) {
             uint4* sw = reinterpret_cast<uint4*>(stage);
             uint4* sx = reinterpret_cast<uint4*>(stage + S::WE);
             const int wbase = tid & ~63;
@@ -355,7 +334,7 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
 #pragma unroll
             for (int i = 0; i < S::XL; ++i) {
                 const int e = i * S::NT + tid;
-                const uint4* g = reinterpret_cast<const uint4*>(xrow(k0 + e / (BN / 2), tb)) + e % (BN / 2);
+                const uint4* g = reinterpret_cast<const uint4*>(xrow(k0 + e / (BN / 2))) + e % (BN / 2);
                 lds_dma16<false>(g, sx + i * S::NT + wbase);
             }
         };
@@ -364,32 +343,23 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
         // barrier).  No register loads happen in this loop, so the compiler
         // has no loads of its own to wait for.
         auto step = [&](int s, float2* cur, float2* ahead) {
-            // this stage's loads are done when at most the memory
-            // instructions issued after them remain (the memory counter
-            // retires in order): the loads of the stages after it.  On the
-            // first stage of a patch block the previous block's output
-            // stores were issued last, so the same wait also covers the
-            // next stage's loads and most of those stores -- it waits
-            // longer than needed, never less.
-            const int later = min(s + PF - 1, total - 1) - s;
+            // this stage's loads are done when at most those of the stages
+            // issued after it remain (the memory counter retires in order)
+            const int later = min(s + PF - 1, nfull - 1) - s;
             if (PF >= 3 && later >= 2) __builtin_amdgcn_s_waitcnt(vmcnt_wait(2 * LPS));
             else if (later == 1) __builtin_amdgcn_s_waitcnt(vmcnt_wait(LPS));
             else __builtin_amdgcn_s_waitcnt(vmcnt_wait(0));
             asm volatile("s_barrier" ::: "memory");
-            if (s + PF < total) dma_stage(s + PF, ahead);
+            if (s + PF < nfull) dma_stage((s + PF) * KC, ahead);
             multiply(cur);
-            if (s + 1 < total && (s + 1) % nfull == 0) {
-                store_tile(s / nfull);
-                zero_acc();
-            }
         };
 #pragma unroll
         for (int d = 0; d < PF; ++d)
-            if (d < total) dma_stage(d, bufs[d]);
-        for (int s0 = 0; s0 < total; s0 += NB) {
+            if (d < nfull) dma_stage(d * KC, bufs[d]);
+        for (int s0 = 0; s0 < nfull; s0 += NB) {
 #pragma unroll
             for (int r = 0; r < NB; ++r)
-                if (s0 + r < total) step(s0 + r, bufs[r], bufs[(r + PF) % NB]);
+                if (s0 + r < nfull) step(s0 + r, bufs[r], bufs[(r + PF) % NB]);
         }
         if (nfull < nstage) {
             // the partial last stage, through registers (masked rows), once
@@ -402,7 +372,8 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
         }
     }
 
-    store_tile(tpw - 1);
+    store_output_tile<TM, TN, G3>(ys, accR, accI, acc3, co0 + wm * (TM * 32), t0 + wn * (TN * 32), f, nbins, ygroup,
+                                  ntp, krow, col, packed);
 }
 
 template <int BM, int BN, int KC, int WM, bool G3 = false, int PF = 1>
@@ -415,11 +386,9 @@ static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, 
     if (attr != hipSuccess) return attr;
     if (p.coutp % BM != 0 || p.ntp % BN != 0) return hipErrorInvalidValue;
     const int nbco = p.coutp / BM, nbt = p.ntp / BN;
-    const int tpw = p.con_tpw;
-    if (tpw < 1 || nbt % tpw != 0 || (tpw > 1 && (PF < 2 || p.prob.cin % KC != 0))) return hipErrorInvalidValue;
-    const size_t nb = size_t(nbco) * nbt * p.bins / tpw;
+    const size_t nb = size_t(nbco) * nbt * p.bins;
     return launch_kernel(kern, dim3(unsigned(nb)), dim3(S::NT), lds, s, ev.start, ev.stop, xs, ws, ys,
-                         p.prob.cin, p.coutp, p.ntp, nbco, nbt, p.bins, patch_group(p.L), packed_slots(p.L), tpw);
+                         p.prob.cin, p.coutp, p.ntp, nbco, nbt, p.bins, patch_group(p.L), packed_slots(p.L));
 }
 
 // The variants launch_contract dispatches (checked at plan time, so that a

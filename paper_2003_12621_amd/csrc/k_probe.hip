@@ -78,11 +78,10 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_probe_matrix(fftsplit_plan_t plan, fl
     const int wm = bm == 128 && bn == 32 ? 4 : (bm == 256 ? 4 : 2);   // the wave grids launch_contract uses
     const int tm = bm / wm / 32, tn = bn / (4 / wm) / 32;
     const int nstage = (plan->prob.cin + kc - 1) / kc;
-    const int tpw = plan->con_tpw;
-    const long long per_wave = (long long)nstage * (kc / 2) * tm * tn * plan->con_products * tpw;
+    const long long per_wave = (long long)nstage * (kc / 2) * tm * tn * plan->con_products;
     const int pf = plan->con_prefetch;
     const int lds = (pf > 1 ? pf + 1 : 2) * kc * (bm + bn) * 8;
-    const long long nb = (long long)(plan->coutp / bm) * (plan->ntp / bn) * plan->bins / tpw;
+    const long long nb = (long long)(plan->coutp / bm) * (plan->ntp / bn) * plan->bins;
     if (nb < 1 || nb > 0x7fffffffLL) return fail(FFTSPLIT_ERROR_NOT_SUPPORTED, "grid size out of range");
     DeviceGuard g(plan->device);
     if (!g.ok()) return fail(FFTSPLIT_ERROR_DEVICE, "cannot select the plan's device");

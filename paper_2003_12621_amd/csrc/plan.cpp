@@ -336,29 +336,6 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
         if (!lds_variant) plan->con_prefetch = 1;
         if (plan->con_prefetch == 3 && plan->con_bm != 64) plan->con_prefetch = 2;
     }
-    // Patch blocks per contraction workgroup (stages loaded ahead through
-    // LDS and whole channel stages only): the largest of 8, 4, 2 that
-    // divides the bin's patch blocks and leaves at least two workgroups per
-    // compute unit, so that a workgroup's next block is loaded while it
-    // finishes the current one.  Measured on the 64- and 128-channel VGG-16
-    // layers: 3-7 % off the contraction; with one workgroup per compute
-    // unit it loses (8 on 8x128x112^2: 94 against 75 us).
-    // FFTSPLIT_CONTRACT_TPW=n forces n (when valid).
-    plan->con_tpw = 1;
-    if (plan->con_prefetch >= 2 && p.cin % plan->con_kc == 0 && g.ntp % plan->con_bn == 0 &&
-        g.coutp % plan->con_bm == 0) {
-        const int nbt = g.ntp / plan->con_bn;
-        const long long nb = (long long)(g.coutp / plan->con_bm) * nbt * g.bins;
-        for (int t = 8; t > 1; t /= 2)
-            if (nbt % t == 0 && nb / t >= 2LL * plan->cus) {
-                plan->con_tpw = t;
-                break;
-            }
-        if (const char* v = std::getenv("FFTSPLIT_CONTRACT_TPW")) {
-            const int t = std::atoi(v);
-            if (t >= 1 && nbt % t == 0) plan->con_tpw = t;
-        }
-    }
     if (g.coutp % plan->con_bm != 0 || g.ntp % plan->con_bn != 0) {
         const int bm = plan->con_bm, bn = plan->con_bn;
         delete plan;
@@ -445,7 +422,6 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_plan_info(fftsplit_plan_t plan, fftsp
     i.spec_group = patch_group(plan->L);
     i.fused_channel_sum = plan->fuse_cin ? 1 : 0;
     i.contract_prefetch = plan->con_prefetch;
-    i.contract_tiles_per_group = plan->con_tpw;
     i.model_contract_flops = plan->model_con_flops;
     i.model_transform_bytes = plan->model_xfer_bytes;
     i.model_seconds = plan->model_seconds;

@@ -307,19 +307,3 @@ def test_probe_argument_checks():
     assert L.fftsplit_probe_stream(ctypes.c_void_p((1 << 20) + 8), b, 16, 16, None) == fs.ERROR_INVALID_VALUE
     assert L.fftsplit_probe_stream(a, ctypes.c_void_p((1 << 20) + 16), 64, 64, None) == fs.ERROR_INVALID_VALUE  # overlap
     assert L.fftsplit_probe_stream(None, None, 0, 0, None) == fs.SUCCESS                  # nothing to do
-
-
-@pytest.mark.parametrize("shape,tile,tpw", [
-    ((32, 64, 224, 224, 64, 3), 14, 8),    # 16384 64x64 tiles: 8 per workgroup leaves 2048 workgroups
-    ((8, 128, 112, 112, 128, 3), 14, 4),   # 2048 tiles: 4 leaves 512 (two per compute unit), 8 would leave 256
-    ((16, 256, 56, 56, 256, 5), 28, 1),    # one patch block per bin
-    ((16, 256, 56, 56, 256, 5), 12, 1),    # 13 patch blocks of 32 per bin: nothing divides
-    ((1, 64, 224, 224, 64, 3), 14, 1),     # 512 tiles: too few to group
-    ((2, 130, 17, 17, 3, 3), 14, 1),       # input channels not a multiple of the stage
-])
-def test_contraction_tiles_per_group(shape, tile, tpw):
-    """The plan groups consecutive patch blocks of a bin per contraction
-    workgroup where that leaves at least two workgroups per compute unit."""
-    n, cin, h, w, cout, k = shape
-    p = fs.Plan(n, cin, h, w, cout, k, tile=tile, arch="gfx950")
-    assert p.info.contract_tiles_per_group == tpw

@@ -363,28 +363,3 @@ def test_large_layer_general_kernels():
         ref = oracle.direct_xcorr2d(xi, wt[sel])
         got = y[img:img + 1, sel].cpu().numpy()
         assert rel_l2(got, ref) <= GATE, img
-
-
-@pytest.mark.parametrize("shape,tile,tpw", [((8, 32, 112, 112, 64, 3), 14, 2), ((32, 16, 56, 56, 64, 3), 14, 8)])
-def test_contraction_tile_grouping(shape, tile, tpw, monkeypatch):
-    """Several patch blocks per contraction workgroup give bit-identical
-    output spectra and output to one block per workgroup (each block's sum
-    over input channels runs in the same order), and match the oracle."""
-    n, cin, h, w, cout, k = shape
-    print(f"[case] tile grouping {shape} T={tile} tpw={tpw}", flush=True)
-    x, wt = small_layer(n, cin, h, w, cout, k, seed=71)
-    outs = {}
-    for t in (1, tpw):
-        monkeypatch.setenv("FFTSPLIT_CONTRACT_TPW", str(t))
-        plan = fs.Plan(n, cin, h, w, cout, k, tile=tile)
-        assert plan.info.contract_tiles_per_group == t
-        ws = plan.new_workspace()
-        wspec = plan.transform_weights(_dev(wt))
-        y = plan.conv2d(_dev(x), wspec, workspace=ws)
-        torch.cuda.synchronize()
-        outs[t] = y.cpu().numpy()
-    monkeypatch.delenv("FFTSPLIT_CONTRACT_TPW")
-    assert np.array_equal(outs[1], outs[tpw])
-    sel = [0, cout // 2, cout - 1]
-    ref = oracle.direct_xcorr2d(x[:2], wt[sel])
-    assert rel_l2(outs[tpw][:2][:, sel], ref) <= GATE
