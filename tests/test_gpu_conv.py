@@ -78,6 +78,12 @@ EDGE = [
     ((1, 5, 23, 300, 7, 3), 30),     # width beyond the row-band kernels' 256: general forward / inverse, L = 32
     ((2, 4, 19, 264, 9, 5), 12),     # the same at L = 16, K = 5
     ((1, 3, 9, 258, 4, 3), 6),       # the same at L = 8
+    ((1, 4, 20, 20, 5, 9), 8),       # K = 9 at L = 16
+    ((2, 3, 17, 23, 4, 15), 2),      # K = 15: two-pixel tiles at L = 16 (overlap-save only)
+    ((1, 2, 40, 40, 3, 31), 2),      # K = 31, the largest kernel: two-pixel tiles at L = 32
+    ((1, 3, 9, 9, 2, 7), 26),        # one tile larger than the image, K = 7
+    ((3, 5, 1, 37, 6, 3), 6),        # one-row images
+    ((2, 4, 29, 1, 3, 5), 12),       # one-column images
 ]
 
 
