@@ -300,8 +300,8 @@ __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux
 // of 4, at most 256; crop width T >= L/2).  Same work items and transforms as inverse_kernel;
 // what changes is the memory traffic and how items overlap:
 //   * the output spectra of item i+1 are loaded into registers while item
-//     i is transformed and stored (streaming loads: nothing reads them
-//     again);
+//     i's rows are transformed and its band is stored (streaming loads:
+//     nothing reads them again);
 //   * the column pass runs one instruction stream in every lane: lane j = 0,
 //     which rebuilds the two Hermitian columns k2 = 0 and k2 = L/2 and packs
 //     them as one complex sequence, does so with selects, so no wave
@@ -508,14 +508,23 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
                 const float2 v1 = k1 < H2 ? pa[k1] : pb[k1 - H2];
                 cz[k1] = j0 ? v0 : v1;
             }
-            // the next item's spectra stay in flight through this item
-            load_spectra(item + 1 < iend ? item + 1 : -1);
+            // NCI > 0: the next item's filter spectra stay in flight
+            // through this whole item
+            if constexpr (NCI > 0) load_spectra(item + 1 < iend ? item + 1 : -1);
             fft<L, true>(cz);
             // lane 0's result is the two real columns packed (column 0 +
             // i * column L/2): it stays packed in slot 0 for the row pass
             float2* cbw = tb + opaque(uc * TTS);
 #pragma unroll
             for (int m = 0; m < L; ++m) cbw[m * TP + jc] = cz[m];
+            // NCI = 0: the next item's output spectra are issued here, after
+            // this item's column transform rather than before it, and stay
+            // in flight through its row pass and store phase.  The registers
+            // they fill are then not live across the column transform (165
+            // instead of 199 at L = 32), and the loads of workgroups whose
+            // first item arrived early compete less with the first loads of
+            // the others.
+            if constexpr (NCI == 0) load_spectra(item + 1 < iend ? item + 1 : -1);
         }
         __syncthreads();
 
