@@ -461,21 +461,29 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
                 gcur = t0;
             }
             __syncthreads();
-            // per-bin channel sum (eq. 9): pa, pb = sum_ci W x
-            auto cmul = [](float2 a, float2 b) { return make_float2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x); };
-            auto pmul = [](float2 a, float2 b) { return make_float2(a.x * b.x, a.y * b.y); };
+            // per-bin channel sum (eq. 9): pa, pb = sum_ci W x, four
+            // multiply-adds per complex product.  The two packed slots
+            // (lane 0, k1 = 0) multiply part by part: (Wr Xr, Wi Xi), the
+            // same multiply-adds with the cross terms' operands zeroed.
+            auto cmac = [](float2 s, float2 w, float2 x, bool packed) {
+                const float xc = packed ? 0.f : x.y;          // cross term of the real part
+                const float xd = packed ? x.y : x.x;          // Wi's partner in the imaginary part
+                s.x = fmaf(w.x, x.x, s.x);
+                s.x = fmaf(-w.y, xc, s.x);
+                s.y = fmaf(w.y, xd, s.y);
+                s.y = fmaf(w.x, xc, s.y);
+                return s;
+            };
 #pragma unroll
             for (int k1 = 0; k1 < H2; ++k1) {
                 float2 sa = make_float2(0.f, 0.f), sb = make_float2(0.f, 0.f);
                 const float2* wa = wl + slot_a(k1) * NCI;
                 const float2* wb = wl + slot_b(k1) * NCI;
+                const bool packed = k1 == 0 && j0;
 #pragma unroll
                 for (int ci = 0; ci < NCI; ++ci) {
-                    // the two packed slots (lane 0, k1 = 0) multiply part by part
-                    const float2 pa_ = (k1 == 0 && j0) ? pmul(wa[ci], xa[ci][k1]) : cmul(wa[ci], xa[ci][k1]);
-                    const float2 pb_ = (k1 == 0 && j0) ? pmul(wb[ci], xb[ci][k1]) : cmul(wb[ci], xb[ci][k1]);
-                    sa = make_float2(sa.x + pa_.x, sa.y + pa_.y);
-                    sb = make_float2(sb.x + pb_.x, sb.y + pb_.y);
+                    sa = cmac(sa, wa[ci], xa[ci][k1], packed);
+                    sb = cmac(sb, wb[ci], xb[ci][k1], packed);
                 }
                 pa[k1] = sa;
                 pb[k1] = sb;
