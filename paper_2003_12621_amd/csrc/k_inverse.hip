@@ -527,11 +527,8 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
             for (int m = 0; m < L; ++m) cbw[m * TP + jc] = cz[m];
             // NCI = 0: the next item's output spectra are issued here, after
             // this item's column transform rather than before it, and stay
-            // in flight through its row pass and store phase.  The registers
-            // they fill are then not live across the column transform (165
-            // instead of 199 at L = 32), and the loads of workgroups whose
-            // first item arrived early compete less with the first loads of
-            // the others.
+            // in flight through its row pass and store phase; the registers
+            // they fill are then not live across the column transform.
             if constexpr (NCI == 0) load_spectra(item + 1 < iend ? item + 1 : -1);
         }
         __syncthreads();
