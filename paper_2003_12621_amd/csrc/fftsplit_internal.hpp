@@ -71,9 +71,16 @@ __host__ __device__ constexpr int patch_group(int L) {
 // 22.5-23.6 -> 20.9-22.4 us on the 16x256x56^2 layer, warm).
 __host__ __device__ constexpr int forward_group(int L) { return L == 32 ? 8 : patch_group(L); }
 
-// Patch stride (float2) of the half spectra in the band variant of the
-// forward transform: L rows of L/2+1 bins, plus one to make it odd.
-__host__ __device__ constexpr int band_half_stride(int L) { return L * (L / 2 + 1) + 1; }
+// Patch stride (float2) of the half spectra in the band transforms, for
+// work items of TG patches: L rows of L/2+1 bins plus a pad that spreads the
+// column pass over the LDS banks.  There, 16 consecutive lanes (one bank
+// sweep of 8-byte accesses over 32 four-byte banks) hold min(TG, 16)
+// patches u and 16 / min(TG, 16) columns j, at float2 index u * stride + j;
+// with L (L/2 + 1) a multiple of 16 at L = 16 and 32, a pad of 16 / TG for
+// TG < 16 and of 1 otherwise puts them in distinct bank pairs.
+__host__ __device__ constexpr int band_half_stride(int L, int TG) {
+    return L * (L / 2 + 1) + (TG < 16 ? 16 / TG : 1);
+}
 
 // Band loads per thread (16 bytes each) the band variant of the forward
 // transform holds in registers, by FFT size.

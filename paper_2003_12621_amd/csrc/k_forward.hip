@@ -224,9 +224,10 @@ __global__ __launch_bounds__(TG * (L / 2)) void forward_kernel(const float* __re
 //     j + L/2 (not 2j and 2j+1); with the odd band pitch the L/2 row-pass
 //     lanes of a patch, which read rows j, hit distinct banks, and with the
 //     odd row stride of the half spectra (L/2+1 float2) its row writes do
-//     too; the patch stride of the half spectra is odd, so the column-pass
-//     reads of a wave's patches spread evenly; the band is written with
-//     4-byte stores (odd rows are not 8-byte aligned).
+//     too; the patch stride of the half spectra (band_half_stride) puts
+//     the column-pass reads of the patches and columns that share a bank
+//     sweep in distinct banks; the band is written with 4-byte stores (odd
+//     rows are not 8-byte aligned).
 template <int L, int TG, int NV>
 __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
     const float* __restrict__ x, float2* __restrict__ xs, int cin, int h, int w, int T, int P, int th, int tw, int nt,
@@ -234,7 +235,7 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
     float inv_th) {
     using S = FwdShape<L, TG>;
     constexpr int NT = S::NT, NW = NT / 64, H2 = S::H2, TP = S::TP;
-    constexpr int TTS = band_half_stride(L);  // half-spectrum patch stride (float2), odd
+    constexpr int TTS = band_half_stride(L, TG);  // half-spectrum patch stride (float2)
     constexpr int F = stored_bins(L);
     extern __shared__ float4 lds_raw[];
     float* band = reinterpret_cast<float*>(lds_raw);

@@ -312,7 +312,8 @@ __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux
 //     of the convolution reads y), lanes along each row, with bias and ReLU;
 //     in the first and last tile row of an item only the columns of its own
 //     tiles are written;
-//   * LDS strides are odd, so the lanes of a wave spread over the banks.
+//   * LDS strides are odd (the half-spectrum patch stride: band_half_stride),
+//     so the lanes of a wave spread over the banks.
 // POOL: the 2x2 max-pool happens in the store phase (FFTSPLIT_MAXPOOL).
 // NCI > 0 (layers with NCI <= 4 input channels): the per-bin channel sum
 // (eq. 9) is done here instead of by the contraction, and the output
@@ -329,7 +330,7 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     unsigned y_bytes, float inv_h, float inv_tw, float inv_th, const float2* __restrict__ xsp,
     const float2* __restrict__ wsp, int cin, int wl_off) {
     constexpr int H2 = L / 2, NT = TG * H2, NW = NT / 64, TP = H2 + 1;
-    constexpr int TTS = band_half_stride(L);  // half-spectrum patch stride (float2), odd
+    constexpr int TTS = band_half_stride(L, TG);  // half-spectrum patch stride (float2)
     constexpr int F = stored_bins(L);
     extern __shared__ float4 lds_raw[];
     float2* tb = reinterpret_cast<float2*>(lds_raw);

@@ -108,7 +108,7 @@ static void choose_inverse_band(fftsplit_plan_s& p) {
     int obp = p.tw * T;
     if (obp % 2 == 0) ++obp;   // odd pitch: a patch's row-pass lanes write distinct banks
     const size_t band = size_t(slots) * obp * 4;
-    const size_t half = size_t(tg) * band_half_stride(L) * 8;
+    const size_t half = size_t(tg) * band_half_stride(L, tg) * 8;
     const size_t lds = band > half ? band : half;
     if (lds > 80 * 1024) return;
     p.inv_band = true;
@@ -145,7 +145,7 @@ static void choose_forward_band(fftsplit_plan_s& p) {
     int bp = co + p.tw * T + P;
     if (bp % 2 == 0) ++bp;   // odd pitch: a patch's row-pass lanes read distinct banks
     const size_t band = size_t(slots + 1) * bp * 4;
-    const size_t half = size_t(tg) * band_half_stride(L) * 8;
+    const size_t half = size_t(tg) * band_half_stride(L, tg) * 8;
     const size_t lds = band > half ? band : half;
     if (lds > 80 * 1024) return;
     p.fwd_band = true;
