@@ -32,9 +32,9 @@
 // while the current pair's MFMAs run.  The filter spectra, the bulk of the
 // bytes, are loaded non-temporally where each block of them is read by one
 // workgroup, so they do not evict the patch and output spectra.  The
-// channel blocks of one bin are consecutive logical workgroups on the same
-// XCD, so the bin's patch spectra are fetched from HBM once and reused from
-// L2.
+// workgroups of one bin run on the same XCD, so the bin's patch spectra
+// are fetched from HBM once and reused from L2, and the bins are dealt to
+// the XCDs in turn, so that together they sweep the spectra in order.
 #include "fftsplit_internal.hpp"
 #include "launch_util.hpp"
 
@@ -195,7 +195,20 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
     const int wave = tid >> 6;
     const int wm = wave / S::WN, wn = wave % S::WN;
 
-    const int lb = xcd_logical_block(blockIdx.x, gridDim.x);
+    // Logical block lb = (bin, patch block, channel block), channel blocks
+    // fastest.  The hardware deals workgroup i to XCD i % 8; the bins are
+    // dealt to the XCDs in turn (bin f to XCD f % 8, its workgroups
+    // consecutive there), so that a bin's workgroups share that XCD's L2
+    // and the XCDs together sweep the bins in order.  Grids that the turns
+    // do not divide keep one contiguous range of bins per XCD.
+    const int per_bin = nbco * nbt;
+    int lb;
+    if (int(gridDim.x) % (kNumXcd * per_bin) == 0) {
+        const int x = int(blockIdx.x) % kNumXcd, j = int(blockIdx.x) / kNumXcd;
+        lb = ((j / per_bin) * kNumXcd + x) * per_bin + j % per_bin;
+    } else {
+        lb = xcd_logical_block(blockIdx.x, gridDim.x);
+    }
     const int cbk = lb % nbco;
     const int rest = lb / nbco;
     const int tbk = rest % nbt;
