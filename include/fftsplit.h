@@ -183,8 +183,11 @@ typedef struct {
  * the measured best): FFTSPLIT_CONTRACT_TILE (see contract_tile_m),
  * FFTSPLIT_CONTRACT_PREFETCH (see contract_prefetch),
  * FFTSPLIT_FORWARD_BAND=0 / FFTSPLIT_INVERSE_BAND=0 (general forward /
- * inverse kernels instead of the row-band ones), FFTSPLIT_FUSE_CIN=0 (no
- * channel sum in the inverse), FFTSPLIT_LOG=1 (print the plan to stderr). */
+ * inverse kernels instead of the row-band ones), FFTSPLIT_FORWARD_SWEEP=1 / 0
+ * (the row-band forward's workgroups run items a grid apart, or contiguous
+ * runs; by default the former where input and patch spectra exceed 256 MB),
+ * FFTSPLIT_FUSE_CIN=0 (no channel sum in the inverse), FFTSPLIT_LOG=1 (print
+ * the plan to stderr). */
 fftsplit_status_t fftsplit_plan(const fftsplit_problem_t* prob, int device, fftsplit_plan_t* out);
 
 /* As fftsplit_plan, but for a named architecture string (host-only, no HIP

@@ -232,7 +232,7 @@ template <int L, int TG, int NV>
 __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
     const float* __restrict__ x, float2* __restrict__ xs, int cin, int h, int w, int T, int P, int th, int tw, int nt,
     int ntp, int ngroups, int nitems, int ipw, int bp, int co, int zslot, unsigned x_bytes, float inv_h, float inv_tw,
-    float inv_th) {
+    float inv_th, int sweep) {
     using S = FwdShape<L, TG>;
     constexpr int NT = S::NT, NW = NT / 64, H2 = S::H2, TP = S::TP;
     constexpr int TTS = band_half_stride(L, TG);  // half-spectrum patch stride (float2)
@@ -259,9 +259,12 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
         return v;
     };
 
-    const int lw = xcd_logical_block(blockIdx.x, gridDim.x);
-    const int ibeg = lw * ipw;
-    const int iend = min(ibeg + ipw, nitems);
+    // sweep: workgroup lw runs items lw, lw + gridDim.x, ...; otherwise a
+    // contiguous run of ipw items, in XCD-aware order
+    const int lw = sweep ? int(blockIdx.x) : xcd_logical_block(blockIdx.x, gridDim.x);
+    const int istep = sweep ? int(gridDim.x) : 1;
+    const int ibeg = sweep ? lw : lw * ipw;
+    const int iend = sweep ? nitems : min(ibeg + ipw, nitems);
 
     float4 v[NV];
     // Slot k of this lane is band row slot0 + k * slot_step.
@@ -336,7 +339,7 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
         write_band(g);
         __syncthreads();
         // the next item's loads stay in flight through this item's transforms
-        load_band(item + 1 < iend ? item + 1 : -1);
+        load_band(item + istep < iend ? item + istep : -1);
 
         // row pass (j fastest across lanes): rows j and j + L/2 of patch u's
         // window (rows a stride of L/2 apart, not adjacent ones, so that with
@@ -432,7 +435,7 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
     if (ibeg < iend) {
         load_band(ibeg);
         process(ibeg);
-        for (int item = ibeg + 1; item < iend; ++item) process(item);
+        for (int item = ibeg + istep; item < iend; item += istep) process(item);
     }
 }
 
@@ -480,7 +483,8 @@ static hipError_t launch_forward_band(const fftsplit_plan_s& p, const float* x, 
     const unsigned x_bytes = unsigned(size_t(p.prob.n) * p.prob.cin * p.prob.h * p.prob.w * 4);
     return launch_kernel(kern, grid, dim3(S::NT), unsigned(lds), s, ev.start, ev.stop, x, xs, p.prob.cin, p.prob.h,
                          p.prob.w, p.T, p.P, p.th, p.tw, p.nt, p.ntp, ngroups, nitems, ipw, p.fwd_bp, p.fwd_co,
-                         p.fwd_zslot, x_bytes, 1.0f / float(p.prob.h), 1.0f / float(p.tw), 1.0f / float(p.th));
+                         p.fwd_zslot, x_bytes, 1.0f / float(p.prob.h), 1.0f / float(p.tw), 1.0f / float(p.th),
+                         p.fwd_sweep ? 1 : 0);
 }
 
 hipError_t launch_forward(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s,

@@ -122,6 +122,7 @@ static void choose_inverse_band(fftsplit_plan_s& p) {
 // per compute unit.  FFTSPLIT_FORWARD_BAND=0 turns it off.
 static void choose_forward_band(fftsplit_plan_s& p) {
     p.fwd_band = false;
+    p.fwd_sweep = false;
     const int w = p.prob.w, L = p.L, T = p.T, P = p.P;
     // (offsets are 32-bit; the tile and row arithmetic uses exact float
     // division, valid below 2^22; stores dropped with an out-of-range
@@ -149,6 +150,15 @@ static void choose_forward_band(fftsplit_plan_s& p) {
     const size_t lds = band > half ? band : half;
     if (lds > 80 * 1024) return;
     p.fwd_band = true;
+    // Where the input and the patch spectra together exceed the 256 MB
+    // last-level cache, both stream from and to HBM: then workgroup lw runs
+    // items lw, lw + grid, ..., so that the workgroups together read one
+    // contiguous range of the input and write one of the spectra at a time.
+    // Otherwise each workgroup runs a contiguous run of items and the XCD
+    // remap keeps neighbouring items, which share halo rows, on one L2.
+    const size_t x_bytes = size_t(p.prob.n) * p.prob.cin * p.prob.h * p.prob.w * 4;
+    p.fwd_sweep = x_bytes + p.xspec_bytes > (size_t(256) << 20);
+    if (const char* e = std::getenv("FFTSPLIT_FORWARD_SWEEP")) p.fwd_sweep = *e == '1';
     p.fwd_bp = bp;
     p.fwd_co = co;
     p.fwd_zslot = slots;

@@ -369,3 +369,31 @@ def test_large_layer_general_kernels():
         ref = oracle.direct_xcorr2d(xi, wt[sel])
         got = y[img:img + 1, sel].cpu().numpy()
         assert rel_l2(got, ref) <= GATE, img
+
+
+SWEEP_CASES = [
+    # (n, cin, h, w, cout, k), tile -- 2560 to 4096 forward work items, so
+    # that every workgroup runs several (at L = 16 not all the same number)
+    ((16, 256, 48, 48, 16, 3), 6),
+    ((16, 256, 56, 60, 24, 3), 14),
+    ((16, 512, 56, 56, 16, 5), 28),
+]
+
+
+@pytest.mark.parametrize("shape,tile", SWEEP_CASES, ids=[f"{s}-T{t}" for s, t in SWEEP_CASES])
+def test_forward_sweep_order(shape, tile, monkeypatch):
+    """The row-band forward with its items a grid apart per workgroup
+    (FFTSPLIT_FORWARD_SWEEP=1) and in contiguous runs (=0) against the
+    oracle; the order changes no arithmetic, so both outputs are identical."""
+    n, cin, h, w, cout, k = shape
+    print(f"[case] forward sweep order {shape} T={tile}", flush=True)
+    x, wt = small_layer(n, cin, h, w, cout, k, seed=111)
+    outs = []
+    for sweep in ("1", "0"):
+        monkeypatch.setenv("FFTSPLIT_FORWARD_SWEEP", sweep)
+        plan = fs.Plan(n, cin, h, w, cout, k, tile=tile)
+        y = plan.conv2d(_dev(x), plan.transform_weights(_dev(wt)))
+        torch.cuda.synchronize()
+        outs.append(y.cpu().numpy())
+    assert rel_l2(outs[0], oracle.direct_xcorr2d(x, wt)) <= GATE
+    assert np.array_equal(outs[0], outs[1])
