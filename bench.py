@@ -381,7 +381,7 @@ def stage_record(counts, fwd, con, inv):
     }
 
 
-def other_layer(name, tile, dev, steps=20, settle_s=0.25):
+def other_layer(name, tile, dev, steps=20, settle_s=0.25, oracle_budget_s=0.0):
     """A short settled measurement of another single layer: step time,
     effective GFLOP/s, images/s and stage fractions, and the oracle's
     rel-L2 on a sample of the output."""
@@ -403,10 +403,12 @@ def other_layer(name, tile, dev, steps=20, settle_s=0.25):
            "fused_channel_sum": bool(run.info.fused_channel_sum),
            "parity_rel_l2": run.parity(x, w, b, slice(0, 1), chans)}
     del run
+    if oracle_budget_s > 0:
+        rec["cpu_oracle"] = cpu_baseline(layer, x, w, b, tile, budget_s=oracle_budget_s)
     return rec
 
 
-def vgg16_summary(dev, steps=10, settle_s=0.5):
+def vgg16_summary(dev, steps=10, settle_s=0.5, oracle_timed=False):
     """The VGG-16 stack at batch 32 (plan-chosen tiles, fused max-pools):
     settled step time, effective GFLOP/s, images/s, per-layer times."""
     import torch
@@ -434,12 +436,19 @@ def vgg16_summary(dev, steps=10, settle_s=0.5):
     # final activation of image 0 against the float64 chain
     import oracle
     got = stack.forward(xd)[:1].cpu().numpy().astype(np.float64)
+    t0 = time.perf_counter()
     ref = oracle.vgg16_forward(x[:1], layers)
-    return {"workload": f"vgg16 conv stack, batch {VGG_BATCH}, 3x224x224, bias+ReLU, 5 max-pools",
+    t_ref = time.perf_counter() - t0
+    rec = {"workload": f"vgg16 conv stack, batch {VGG_BATCH}, 3x224x224, bias+ReLU, 5 max-pools",
             "tiles": stack.tiles, "steps": steps, "ms_per_step": round(ms, 4),
             "GFLOP/s": round(flops / (ms * 1e-3) / 1e9, 1), "images_per_s": round(VGG_BATCH / (ms * 1e-3), 1),
             "layer_ms": layer_ms,
             "parity_rel_l2_image0": float(np.linalg.norm(got - ref) / np.linalg.norm(ref))}
+    if oracle_timed:
+        rec["cpu_oracle"] = {"value": round(flops / VGG_BATCH / t_ref / 1e9, 3), "unit": "GFLOP/s", "kind": "oracle",
+                             "sample": f"oracle.vgg16_forward (float64 numpy, direct cross-correlation per layer) "
+                                       f"on 1 of {VGG_BATCH} images, {t_ref:.1f} s; {1.0 / t_ref:.3f} images/s"}
+    return rec
 
 
 def bench_vgg16(args):
@@ -601,6 +610,9 @@ def main():
                          "the matrix probe of the contraction's launch")
     ap.add_argument("--no-others", action="store_true",
                     help="skip the other workloads (the other single layers and the VGG-16 stack)")
+    ap.add_argument("--oracle-all", action="store_true",
+                    help="also time the CPU oracle (split and direct) on a bounded sample of each other workload "
+                         "and the VGG-16 stack (about a minute of host time; off by default)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="before timing, copy a buffer of this many MiB 3 times (calibrates HBM counters)")
     args = ap.parse_args()
@@ -737,9 +749,9 @@ def main():
         for name, t in OTHER_LAYERS:
             if name == args.config and t == tile:
                 continue
-            others[f"{name}_T{t}"] = other_layer(name, t, dev)
+            others[f"{name}_T{t}"] = other_layer(name, t, dev, oracle_budget_s=6.0 if args.oracle_all else 0.0)
             torch.cuda.empty_cache()
-        others["vgg16_b32"] = vgg16_summary(dev)
+        others["vgg16_b32"] = vgg16_summary(dev, oracle_timed=args.oracle_all)
         out["workloads"] = others
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layer, x, w, b, tile)
