@@ -216,10 +216,13 @@ __global__ __launch_bounds__(TG * (L / 2)) void forward_kernel(const float* __re
 //     LDS with `co` zero columns on the left and zeros up to the pitch `bp`
 //     on the right; a zero row (slot `zslot`) stands in for rows outside
 //     the image.  The row pass cuts each patch's L x L window out of it;
-//   * pipelining: the band loads of item i+1 are issued into registers
-//     before item i is transformed, and item i's spectra are stored
-//     straight from the column pass, so loads, transforms and stores of
-//     neighbouring items overlap;
+//   * pipelining: the band loads of a workgroup's next item are issued into
+//     registers before the current item is transformed, and its spectra
+//     are stored straight from the column pass, so loads, transforms and
+//     stores of neighbouring items overlap; `sweep` (set by the plan where
+//     input and spectra exceed the last-level cache) spaces a workgroup's
+//     items a grid apart, so the workgroups sweep input and spectra in
+//     order, otherwise a workgroup runs a contiguous run of items;
 //   * LDS banks (32 four-byte banks): the row pass pairs rows j and
 //     j + L/2 (not 2j and 2j+1); with the odd band pitch the L/2 row-pass
 //     lanes of a patch, which read rows j, hit distinct banks, and with the
