@@ -168,6 +168,13 @@ typedef struct {
     double model_contract_flops;
     double model_transform_bytes;
     double model_seconds;
+    /* Transform kernel variants: 1 if the forward / inverse stage runs the
+     * row-band kernel (overlap-save, image width a multiple of 4 and at most
+     * 256), else the general one; forward_sweep is 1 if the row-band forward
+     * spaces each workgroup's work items a grid apart (chosen where the
+     * input and the patch spectra together exceed 256 MB;
+     * FFTSPLIT_FORWARD_SWEEP=1 / 0 forces it at plan time). */
+    int forward_band, forward_sweep, inverse_band;
 } fftsplit_plan_info_t;
 
 /* Validate `prob` (host) and create a plan for `device` (a HIP ordinal).

@@ -60,7 +60,8 @@ class PlanInfo(ctypes.Structure):
                 ("spec_group", ctypes.c_int), ("fused_channel_sum", ctypes.c_int),
                 ("direct_wspec_bytes", ctypes.c_size_t), ("contract_prefetch", ctypes.c_int),
                 ("model_contract_flops", ctypes.c_double), ("model_transform_bytes", ctypes.c_double),
-                ("model_seconds", ctypes.c_double)]
+                ("model_seconds", ctypes.c_double),
+                ("forward_band", ctypes.c_int), ("forward_sweep", ctypes.c_int), ("inverse_band", ctypes.c_int)]
 
 
 class FftsplitError(RuntimeError):

@@ -307,3 +307,50 @@ def test_probe_argument_checks():
     assert L.fftsplit_probe_stream(ctypes.c_void_p((1 << 20) + 8), b, 16, 16, None) == fs.ERROR_INVALID_VALUE
     assert L.fftsplit_probe_stream(a, ctypes.c_void_p((1 << 20) + 16), 64, 64, None) == fs.ERROR_INVALID_VALUE  # overlap
     assert L.fftsplit_probe_stream(None, None, 0, 0, None) == fs.SUCCESS                  # nothing to do
+
+
+@pytest.mark.skipif(not os.path.isdir("/opt/rocm/include"), reason="no HIP headers")
+def test_struct_layouts_match_header(tmp_path):
+    """The binding's ctypes structures have the header's layout: a C program
+    built here against include/fftsplit.h prints sizeof and every field's
+    offsetof, which must equal ctypes' (a mismatch would garble fields
+    silently)."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    structs = {"fftsplit_plan_info_t": fs.PlanInfo, "fftsplit_problem_t": fs.Problem}
+    lines = []
+    for cname, cls in structs.items():
+        lines.append(f'printf("%zu\\n", sizeof({cname}));')
+        lines += [f'printf("%zu\\n", offsetof({cname}, {f}));' for f, _ in cls._fields_]
+    src = tmp_path / "layout.c"
+    src.write_text("#include <stddef.h>\n#include <stdio.h>\n#include \"fftsplit.h\"\nint main(void) {\n"
+                   + "\n".join(lines) + "\nreturn 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-x", "c", "-std=c11", "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include",
+                    "-D__HIP_PLATFORM_AMD__", str(src), "-o", str(exe)], check=True, capture_output=True)
+    got = [int(v) for v in subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split()]
+    want = []
+    for cls in structs.values():
+        want.append(ctypes.sizeof(cls))
+        want += [getattr(cls, f).offset for f, _ in cls._fields_]
+    assert got == want
+
+
+def test_transform_variant_choice(monkeypatch):
+    """Row-band transforms where the width allows them; the forward's items
+    a grid apart only where input and patch spectra exceed 256 MB (the
+    VGG-16 layer 2 at batch 32: 411 + 537 MB), contiguous runs otherwise;
+    the environment forces either."""
+    big = plan(n=32, cin=64, h=224, w=224, cout=64, k=3, tile=14).info
+    assert (big.forward_band, big.forward_sweep, big.inverse_band) == (1, 1, 1)
+    k5 = plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info
+    assert (k5.forward_band, k5.forward_sweep, k5.inverse_band) == (1, 0, 1)
+    narrow = plan(n=32, cin=512, h=14, w=14, cout=512, k=3, tile=14).info   # width not a multiple of 4
+    assert (narrow.forward_band, narrow.forward_sweep, narrow.inverse_band) == (0, 0, 0)
+    monkeypatch.setenv("FFTSPLIT_FORWARD_SWEEP", "1")
+    assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.forward_sweep == 1
+    monkeypatch.setenv("FFTSPLIT_FORWARD_SWEEP", "0")
+    assert plan(n=32, cin=64, h=224, w=224, cout=64, k=3, tile=14).info.forward_sweep == 0
