@@ -398,3 +398,19 @@ def test_forward_sweep_order(shape, tile, monkeypatch):
         outs.append(y.cpu().numpy())
     assert rel_l2(outs[0], oracle.direct_xcorr2d(x, wt)) <= GATE
     assert np.array_equal(outs[0], outs[1])
+
+
+def test_pooled_inverse_uneven_item_counts():
+    """Bias, ReLU and the fused 2x2 max-pool on a layer whose inverse runs
+    2560 work items, three per workgroup but not on every workgroup (items a
+    grid apart), against the oracle."""
+    n, cin, h, w, cout, k, tile = 16, 64, 56, 60, 256, 3, 14
+    print(f"[case] pooled inverse, uneven items ({n},{cin},{h},{w},{cout},{k}) T={tile}", flush=True)
+    x, wt = small_layer(n, cin, h, w, cout, k, seed=121)
+    b = make_random_bias(cout, cin, k, seed=122)
+    plan = fs.Plan(n, cin, h, w, cout, k, tile=tile, bias=True, relu=True, pool=True)
+    assert plan.info.inverse_band == 1
+    y = plan.conv2d(_dev(x), plan.transform_weights(_dev(wt)), _dev(b))
+    torch.cuda.synchronize()
+    ref = oracle.maxpool2x2(oracle.direct_xcorr2d(x, wt, b, relu=True))
+    assert rel_l2(y.cpu().numpy(), ref) <= GATE
