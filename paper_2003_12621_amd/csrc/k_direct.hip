@@ -136,7 +136,7 @@ __global__ __launch_bounds__(256) void direct_kernel(const float* __restrict__ x
             const int co = co0 + wm * 32 + 8 * (r >> 2) + 4 * krow + (r & 3);
             if (co < cout) {
                 float v = acc[r] + (bias ? bias[co] : 0.f);
-                if (relu) v = fmaxf(v, 0.f);
+                if (relu) v = vmax(v, 0.f);
                 y[(size_t(img) * cout + co) * hw + rem] = v;
             }
         }

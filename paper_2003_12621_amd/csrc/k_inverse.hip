@@ -192,7 +192,7 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
                 for (int mb = 0; mb < L; mb += S::MS) {
                     const int m = mb + ms;
                     float v = s[m * SP + q] + bv;
-                    if (relu) v = fmaxf(v, 0.f);
+                    if (relu) v = vmax(v, 0.f);
                     const unsigned vo = (m < ro && q < cw) ? vq + unsigned(m * w) * 4u : kOutOfRange;
                     buf_store_f32(v, ry_out, vo, 0);
                 }
@@ -205,7 +205,7 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
                     if (m < cs && q < cs) {
                         if (m < ro && q < cw) {
                             float v = zv + bv;
-                            if (relu) v = fmaxf(v, 0.f);
+                            if (relu) v = vmax(v, 0.f);
                             y[d + m * w + q] = v;
                         }
                     } else {
@@ -290,7 +290,7 @@ __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc += v[i][j];
         float o = acc + bv;
-        if (relu) o = fmaxf(o, 0.f);
+        if (relu) o = vmax(o, 0.f);
         if (out[i] >= 0) yp[out[i]] = o;
     }
 }
@@ -316,7 +316,8 @@ __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux
 //     tiles are written;
 //   * LDS strides are odd (the half-spectrum patch stride: band_half_stride),
 //     so the lanes of a wave spread over the banks.
-// POOL: the 2x2 max-pool happens in the store phase (FFTSPLIT_MAXPOOL).
+// POOL: the 2x2 max-pool happens in the store phase (FFTSPLIT_MAXPOOL), and
+// ReLU after it.
 // NCI > 0 (layers with NCI <= 4 input channels): the per-bin channel sum
 // (eq. 9) is done here instead of by the contraction, and the output
 // spectra are never stored: each item forms its spectra from the patch
@@ -571,13 +572,12 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
             }
             __syncthreads();  // the output band reuses the half-spectrum LDS
             fft<L, true>(z);
-            // ReLU here, on values the transform has just computed, not in
-            // the store phase (where values read back from LDS would each
-            // need a NaN quieting before the max); with the max-pool the
-            // order does not matter: relu(max(.)) = max(relu(.))
-            if (relu) {
+            // ReLU on the transform's results; with the max-pool it comes
+            // after the pooling instead (relu(max(.)) = max(relu(.)), on a
+            // quarter of the values)
+            if (!POOL && relu) {
 #pragma unroll
-                for (int q = 0; q < L; ++q) z[q] = make_float2(fmaxf(z[q].x, 0.f), fmaxf(z[q].y, 0.f));
+                for (int q = 0; q < L; ++q) z[q] = make_float2(vmax(z[q].x, 0.f), vmax(z[q].y, 0.f));
             }
             const int t = t0 + u;
             if (t < nt && j < T) {
@@ -652,9 +652,12 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
                                    unsigned(sl0 * wp * 4) + unsigned(8 * c4) + unsigned(qd) * crossp;
             const unsigned dq_off = unsigned(dqp) * crossp;
             const float* src = ob + 2 * sl0 * obp + 4 * c4;
+            // 2x2 maximum, then ReLU: with -inf as the floor (no ReLU) the
+            // second maximum leaves its other operands as they are
+            const float lo = relu ? 0.f : -__builtin_inff();
             auto pool4 = [&](const float* sp) {
-                return make_float2(fmaxf(fmaxf(sp[0], sp[1]), fmaxf(sp[obp], sp[obp + 1])),
-                                   fmaxf(fmaxf(sp[2], sp[3]), fmaxf(sp[obp + 2], sp[obp + 3])));
+                return make_float2(vmax3(vmax3(sp[0], sp[1], sp[obp]), sp[obp + 1], lo),
+                                   vmax3(vmax3(sp[2], sp[3], sp[obp + 2]), sp[obp + 3], lo));
             };
             {
                 // batches of SB pooled slots, LDS reads before stores

@@ -159,7 +159,7 @@ __global__ __launch_bounds__(256) void oaa_inverse_kernel(const float2* __restri
                 const int r = a * T + P, cc = b * T + P;
                 if (r < h && cc < w) {
                     float v = acc + (bias ? bias[co] : 0.f);
-                    if (relu) v = fmaxf(v, 0.f);
+                    if (relu) v = vmax(v, 0.f);
                     y[((size_t(img) * cout + co) * h + r) * w + cc] = v;
                 }
             } else {

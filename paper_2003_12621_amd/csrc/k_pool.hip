@@ -15,9 +15,7 @@ __global__ __launch_bounds__(256) void maxpool_kernel(const float* __restrict__ 
     const int i = int(r % ho);
     const size_t plane = r / ho;
     const float* p = x + (plane * h + 2 * i) * w + 2 * j;
-    const float a = fmaxf(p[0], p[1]);
-    const float b = fmaxf(p[w], p[w + 1]);
-    y[idx] = fmaxf(a, b);
+    y[idx] = vmax(vmax3(p[0], p[1], p[w]), p[w + 1]);
 }
 
 hipError_t launch_maxpool(const float* x, float* y, int n, int c, int h, int w, hipStream_t s, hipEvent_t stop) {

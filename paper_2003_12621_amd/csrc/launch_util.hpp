@@ -110,6 +110,15 @@ __device__ __forceinline__ void buf_store_f32x2(float2 v, BufRsrc r, unsigned vo
     __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(int2v, v), r, voff, soff, CP);
 }
 
+// Maximum of two or three floats for ReLU and the max-pool, as IEEE 754-2019
+// `maximum` (a NaN operand gives NaN, as numpy's maximum does).  gfx950 has
+// it as one instruction (v_maximum3_f32) for up to three operands; fmaxf
+// (IEEE maxNum) costs an extra instruction per operand that the compiler
+// cannot prove quiet, which is every value read from memory or computed
+// in another basic block.
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+__device__ __forceinline__ float vmax3(float a, float b, float c) { return vmax(vmax(a, b), c); }
+
 // Optional timing events of one entry-point call: `start` is recorded when
 // the call's first kernel begins and `stop` when its last kernel ends
 // (hipExtLaunchKernel timestamps, no separate event packets).
