@@ -380,9 +380,18 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
         }
     };
 
-    // column-pass roles: patch uc (fastest across lanes), column j
-    const int uc = tid % TG;
-    const int jc = tid / TG;
+    // column-pass roles: patch uc, column jc.  With patch pairs (kPair,
+    // TG <= 32) lanes l and l + 32 of a wave take patches 2 pm and 2 pm + 1
+    // of one column, so that one 16-byte load per lane serves both
+    // (load_spectra); 16 consecutive lanes hold 8 pairs x 2 columns, so the
+    // column pass's LDS writes (odd patch stride TTS) fall in distinct
+    // banks.  Otherwise the patch is the fastest index across lanes.
+    constexpr bool kPair = NCI == 0 && TG <= 32;
+    constexpr int CPW = 64 / TG;   // columns per wave with patch pairs
+    const int hiw = lane >> 5;   // upper half-wave
+    const int pm = (((lane & 31) >> 3) / CPW) * 8 + (lane & 7);
+    const int uc = kPair ? 2 * pm + hiw : tid % TG;
+    const int jc = kPair ? wv * CPW + ((lane & 31) >> 3) % CPW : tid / TG;
     const bool j0 = jc == 0;
     // Lane jc >= 1 needs column k2 = jc: pa[k1] = bin (k1, jc) and
     // pb[k1] = bin (k1 + L/2, jc), k1 < L/2.  Lane 0 needs the halves
@@ -390,6 +399,9 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     // two slots of their real bins, pa[k1] and pb[k1] (k1 >= 1) their
     // complex bins k1.
     float2 pa[H2], pb[H2];
+    // kPair: the loaded 16-byte pairs, (pa, pb) of patch 2 pm in the lower
+    // half-wave's (x, y) and the upper's (z, w) once exchanged
+    float4 pq[kPair ? H2 : 1];
     // slot of pa[k1] / pb[k1] in this lane's column
     auto slot_a = [&](int k1) { return j0 ? (k1 == 0 ? bin_real_a(L) : bin_col0(L, k1)) : bin_mid(L, k1, jc); };
     auto slot_b = [&](int k1) { return j0 ? (k1 == 0 ? bin_real_b(L) : bin_colh(L, k1)) : bin_mid(L, k1 + H2, jc); };
@@ -434,6 +446,20 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
             return;
         }
         // item = co * ngroups + t0 / TG: the item's run starts at item * F * TG
+        if constexpr (kPair) {
+            // lanes l < 32 read the a bins, lanes l + 32 the b bins, each
+            // 16 bytes: patches 2 pm and 2 pm + 1 (8 lanes cover the
+            // group's 128-byte run of one bin)
+            const unsigned pair8 = unsigned(yspec_offset(co, 0, t0 + 2 * opaque(pm), F, TG, ngroups)) * 8u;
+            const int s0 = hiw ? (j0 ? bin_real_b(L) : bin_mid(L, H2, jc)) : (j0 ? bin_real_a(L) : bin_mid(L, 0, jc));
+            const int s1 = hiw ? (j0 ? bin_colh(L, 1) - 1 : bin_mid(L, H2, jc)) : (j0 ? bin_col0(L, 1) - 1 : bin_mid(L, 0, jc));
+            const unsigned v0 = ok ? pair8 + unsigned(s0) * bs8 : kOutOfRange;
+            const unsigned v1 = ok ? pair8 + unsigned(s1) * bs8 : kOutOfRange;
+            pq[0] = buf_load_f32x4<kCacheStream>(ry, v0, 0);
+#pragma unroll
+            for (int k1 = 1; k1 < H2; ++k1) pq[k1] = buf_load_f32x4<kCacheStream>(ry, v1, unsigned(k1) * bs8);
+            return;
+        }
         const unsigned lane8 = unsigned(yspec_offset(co, 0, t0 + opaque(uc), F, TG, ngroups)) * 8u;
         const unsigned va0 = ok ? lane8 + unsigned(j0 ? bin_real_a(L) : bin_mid(L, 0, jc)) * bs8 : kOutOfRange;
         const unsigned vb0 = ok ? lane8 + unsigned(j0 ? bin_real_b(L) : bin_mid(L, H2, jc)) * bs8 : kOutOfRange;
@@ -462,6 +488,20 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
         int co, t0;
         decode(item, co, t0);
         const BandGeom g = band_geom(t0, TG, nt, h, T, 0, th, tw);
+        if constexpr (kPair) {
+            // the lower half-wave holds (a, a') of patches (2 pm, 2 pm + 1),
+            // the upper (b, b'): swapping the lower's second value with the
+            // upper's first leaves each lane (a, b) of its own patch
+#pragma unroll
+            for (int k1 = 0; k1 < H2; ++k1) {
+                const auto sx = __builtin_amdgcn_permlane32_swap(__float_as_uint(pq[k1].x),
+                                                                 __float_as_uint(pq[k1].z), false, false);
+                const auto sy = __builtin_amdgcn_permlane32_swap(__float_as_uint(pq[k1].y),
+                                                                 __float_as_uint(pq[k1].w), false, false);
+                pa[k1] = make_float2(__uint_as_float(sx[0]), __uint_as_float(sy[0]));
+                pb[k1] = make_float2(__uint_as_float(sx[1]), __uint_as_float(sy[1]));
+            }
+        }
         if constexpr (NCI > 0) {
             // the item's filter spectra into LDS, the next item's loaded,
             // the patch group's spectra loaded when the group changes

@@ -84,8 +84,9 @@ __device__ __forceinline__ float2 buf_load_f32x2(BufRsrc r, unsigned voff, unsig
     typedef int int2v __attribute__((ext_vector_type(2)));
     return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, CP));
 }
+template <int CP = kCacheDefault>
 __device__ __forceinline__ float4 buf_load_f32x4(BufRsrc r, unsigned voff, unsigned soff) {
-    return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+    return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, CP));
 }
 // A store of more than 8 bytes needs one wait state before a VALU
 // instruction may overwrite its data registers.  The compiler's hazard model
