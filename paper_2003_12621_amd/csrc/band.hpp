@@ -50,6 +50,40 @@ __host__ __device__ inline int band_slot(const BandGeom& g, int h, int s, int r)
     return s == 0 ? r - g.r0 : g.rows0 + (s - 1) * h + r;
 }
 
+// Column-pass lane roles of the band transforms with patch pairs (work
+// items of TG <= 32 patches, TG / 2 pairs): lanes l and l + 32 of a wave take
+// patches 2 pm and 2 pm + 1 of the same column, so that one 16-byte access
+// of the spectra, whose patches are consecutive in memory, serves both
+// lanes after a v_permlane32_swap (swap_halves).  Within each group of 16
+// consecutive lanes, min(TG / 2, 8) pairs are fastest, then the columns: with
+// the odd (or 2 mod 16) patch stride of the half spectra in LDS, the
+// group's 8-byte accesses of one row then fall in 16 distinct bank pairs.
+template <int TG>
+struct PairRole {
+    static constexpr int P = TG / 2, Q = P < 8 ? P : 8, CPW = 64 / TG;
+    static_assert(TG <= 32 && TG % 2 == 0, "patch pairs need work items of at most 32 patches");
+    int pm, hi, patch, col;
+    __device__ PairRole(int lane, int wave) {
+        const int r = lane & 31, s = r / Q;
+        hi = lane >> 5;
+        pm = (s / CPW) * Q + r % Q;
+        patch = 2 * pm + hi;
+        col = wave * CPW + s % CPW;
+    }
+};
+
+// Exchanges the upper half-wave's a with the lower half-wave's b (one
+// v_permlane32_swap per 32-bit component).  From per-lane values (a, b) of
+// patches 2 pm (lane l < 32) and 2 pm + 1 (lane l + 32) it leaves lane l
+// both patches' a and lane l + 32 both patches' b, each a 16-byte run in
+// patch order; applied to such runs it restores the per-lane values.
+__device__ __forceinline__ void swap_halves(float2& a, float2& b) {
+    const auto sx = __builtin_amdgcn_permlane32_swap(__float_as_uint(a.x), __float_as_uint(b.x), false, false);
+    const auto sy = __builtin_amdgcn_permlane32_swap(__float_as_uint(a.y), __float_as_uint(b.y), false, false);
+    a = make_float2(__uint_as_float(sx[0]), __uint_as_float(sy[0]));
+    b = make_float2(__uint_as_float(sx[1]), __uint_as_float(sy[1]));
+}
+
 // n / d for 0 <= n < 2^22 and d >= 1 with inv_d = 1.0f / d: the float
 // product is within 1/2 of n / d, so one correction step is exact.
 __device__ __forceinline__ int div_small(int n, int d, float inv_d) {

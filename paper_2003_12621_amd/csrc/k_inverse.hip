@@ -381,17 +381,14 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
     };
 
     // column-pass roles: patch uc, column jc.  With patch pairs (kPair,
-    // TG <= 32) lanes l and l + 32 of a wave take patches 2 pm and 2 pm + 1
+    // band.hpp) lanes l and l + 32 of a wave take patches 2 pm and 2 pm + 1
     // of one column, so that one 16-byte load per lane serves both
-    // (load_spectra); 16 consecutive lanes hold 8 pairs x 2 columns, so the
-    // column pass's LDS writes (odd patch stride TTS) fall in distinct
-    // banks.  Otherwise the patch is the fastest index across lanes.
+    // (load_spectra).  Otherwise the patch is the fastest index across lanes.
     constexpr bool kPair = NCI == 0 && TG <= 32;
-    constexpr int CPW = 64 / TG;   // columns per wave with patch pairs
-    const int hiw = lane >> 5;   // upper half-wave
-    const int pm = (((lane & 31) >> 3) / CPW) * 8 + (lane & 7);
-    const int uc = kPair ? 2 * pm + hiw : tid % TG;
-    const int jc = kPair ? wv * CPW + ((lane & 31) >> 3) % CPW : tid / TG;
+    const PairRole<kPair ? TG : 32> pr(lane, wv);
+    const int hiw = pr.hi, pm = pr.pm;
+    const int uc = kPair ? pr.patch : tid % TG;
+    const int jc = kPair ? pr.col : tid / TG;
     const bool j0 = jc == 0;
     // Lane jc >= 1 needs column k2 = jc: pa[k1] = bin (k1, jc) and
     // pb[k1] = bin (k1 + L/2, jc), k1 < L/2.  Lane 0 needs the halves
@@ -489,17 +486,14 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
         decode(item, co, t0);
         const BandGeom g = band_geom(t0, TG, nt, h, T, 0, th, tw);
         if constexpr (kPair) {
-            // the lower half-wave holds (a, a') of patches (2 pm, 2 pm + 1),
-            // the upper (b, b'): swapping the lower's second value with the
-            // upper's first leaves each lane (a, b) of its own patch
+            // the lower half-wave holds the a bins of patches (2 pm,
+            // 2 pm + 1), the upper their b bins: one exchange leaves each
+            // lane (a, b) of its own patch
 #pragma unroll
             for (int k1 = 0; k1 < H2; ++k1) {
-                const auto sx = __builtin_amdgcn_permlane32_swap(__float_as_uint(pq[k1].x),
-                                                                 __float_as_uint(pq[k1].z), false, false);
-                const auto sy = __builtin_amdgcn_permlane32_swap(__float_as_uint(pq[k1].y),
-                                                                 __float_as_uint(pq[k1].w), false, false);
-                pa[k1] = make_float2(__uint_as_float(sx[0]), __uint_as_float(sy[0]));
-                pb[k1] = make_float2(__uint_as_float(sx[1]), __uint_as_float(sy[1]));
+                pa[k1] = make_float2(pq[k1].x, pq[k1].y);
+                pb[k1] = make_float2(pq[k1].z, pq[k1].w);
+                swap_halves(pa[k1], pb[k1]);
             }
         }
         if constexpr (NCI > 0) {
