@@ -304,6 +304,10 @@ __global__ __launch_bounds__(256) void seam_kernel(const float* __restrict__ aux
 //     is stored (streaming loads: nothing reads them again); a workgroup's
 //     items are gridDim.x apart, so the workgroups sweep the spectra and
 //     the output in order;
+//   * at TG <= 32 the spectra are read in 16-byte patch pairs: lanes l and
+//     l + 32 of a wave hold patches 2m and 2m + 1 of one column (PairRole,
+//     band.hpp), each loads one bin of both, and one exchange of the
+//     half-waves (swap_halves) gives every lane its own patch;
 //   * the column pass runs one instruction stream in every lane: lane j = 0,
 //     which rebuilds the two Hermitian columns k2 = 0 and k2 = L/2 and packs
 //     them as one complex sequence, does so with selects, so no wave
