@@ -56,8 +56,9 @@ __host__ __device__ inline int band_slot(const BandGeom& g, int h, int s, int r)
 // of the spectra, whose patches are consecutive in memory, serves both
 // lanes after a v_permlane32_swap (swap_halves).  Within each group of 16
 // consecutive lanes, min(TG / 2, 8) pairs are fastest, then the columns: with
-// the odd (or 2 mod 16) patch stride of the half spectra in LDS, the
-// group's 8-byte accesses of one row then fall in 16 distinct bank pairs.
+// an odd patch stride of the half spectra in LDS (TG >= 16; at TG = 8 a
+// stride of 2 mod 16), the group's 8-byte accesses of one row then fall in
+// 16 distinct bank pairs.
 template <int TG>
 struct PairRole {
     static constexpr int P = TG / 2, Q = P < 8 ? P : 8, CPW = 64 / TG;

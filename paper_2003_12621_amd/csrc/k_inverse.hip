@@ -449,8 +449,8 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
         // item = co * ngroups + t0 / TG: the item's run starts at item * F * TG
         if constexpr (kPair) {
             // lanes l < 32 read the a bins, lanes l + 32 the b bins, each
-            // 16 bytes: patches 2 pm and 2 pm + 1 (8 lanes cover the
-            // group's 128-byte run of one bin)
+            // 16 bytes: patches 2 pm and 2 pm + 1 (each 8 consecutive lanes
+            // read 128 contiguous bytes of one bin)
             const unsigned pair8 = unsigned(yspec_offset(co, 0, t0 + 2 * opaque(pm), F, TG, ngroups)) * 8u;
             const int s0 = hiw ? (j0 ? bin_real_b(L) : bin_mid(L, H2, jc)) : (j0 ? bin_real_a(L) : bin_mid(L, 0, jc));
             const int s1 = hiw ? (j0 ? bin_colh(L, 1) - 1 : bin_mid(L, H2, jc)) : (j0 ? bin_col0(L, 1) - 1 : bin_mid(L, 0, jc));
