@@ -409,7 +409,7 @@ static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, 
 bool contract_variant_exists(int bm, int bn, int kc, int products) {
     const int v = bm * 1000000 + bn * 1000 + kc;
     if (bm <= 0 || bn <= 0 || kc <= 0) return false;
-    if (products == 3) return v == 64064016 || v == 128064016 || v == 64128016 || v == 128032016;
+    if (products == 3) return v == 64064016 || v == 64064008 || v == 128064016 || v == 64128016 || v == 128032016;
     if (products == 4)
         return v == 64064016 || v == 64064032 || v == 128064016 || v == 128064032 || v == 64128016 ||
                v == 128128016 || v == 256064016 || v == 128032016;
@@ -425,6 +425,10 @@ hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xs, const flo
                 if (p.con_prefetch == 2) return launch_contract_v<64, 64, 16, 2, true, 2>(p, xs, ws, ys, s, ev);
                 if (p.con_prefetch == 3) return launch_contract_v<64, 64, 16, 2, true, 3>(p, xs, ws, ys, s, ev);
                 return launch_contract_v<64, 64, 16, 2, true>(p, xs, ws, ys, s, ev);
+            case 64064008:
+                if (p.con_prefetch == 3) return launch_contract_v<64, 64, 8, 2, true, 3>(p, xs, ws, ys, s, ev);
+                if (p.con_prefetch == 2) return launch_contract_v<64, 64, 8, 2, true, 2>(p, xs, ws, ys, s, ev);
+                return launch_contract_v<64, 64, 8, 2, true>(p, xs, ws, ys, s, ev);
             case 128064016:
                 if (p.con_prefetch == 2) return launch_contract_v<128, 64, 16, 2, true, 2>(p, xs, ws, ys, s, ev);
                 return launch_contract_v<128, 64, 16, 2, true>(p, xs, ws, ys, s, ev);

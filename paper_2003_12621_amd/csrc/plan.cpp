@@ -299,21 +299,31 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
     plan->ws_bytes = plan->aux_off + plan->aux_bytes;
 
     // Contraction variant: 64x64 tiles (128x32 where the patches are padded
-    // to 32 only), 16-channel stages, three real products per complex
+    // to 32 only), 16-channel stages (8-channel ones for few input channels
+    // and many workgroups, below), three real products per complex
     // multiply-add (fastest measured on every layer shape);
-    // FFTSPLIT_CONTRACT_TILE=[g3:|g4:]BMxBNxKC overrides.
+    // FFTSPLIT_CONTRACT_TILE=[g3:|g4:]BMxBNxKC and FFTSPLIT_CONTRACT_PREFETCH
+    // override.
     plan->con_bm = g.ntp % 64 == 0 ? 64 : 128;
     plan->con_bn = g.ntp % 64 == 0 ? 64 : 32;
     plan->con_kc = 16;
     plan->con_products = 3;
     // two stages ahead, through LDS (the tiles that have that variant)
     plan->con_prefetch = 2;
-    if (const char* v = std::getenv("FFTSPLIT_CONTRACT_PREFETCH")) {
-        const int pf = std::atoi(v);
-        if (pf >= 1 && pf <= 3) plan->con_prefetch = pf;
+    // Few input channels and many workgroups (at most 8 stages of 16 per
+    // workgroup, at least 8192 64x64 workgroups: the 224^2 and 112^2 VGG-16
+    // layers): each workgroup's first stages, loaded before it can multiply,
+    // are a large part of its time, and 8-channel stages three ahead (32 KB
+    // of LDS, four workgroups per CU instead of three) hide more of them.
+    if (plan->con_bm == 64 && p.cin <= 128 &&
+        size_t(g.coutp / 64) * size_t(g.ntp / 64) * size_t(g.bins) >= 8192) {
+        plan->con_kc = 8;
+        plan->con_prefetch = 3;
     }
+    const char* pf_env = std::getenv("FFTSPLIT_CONTRACT_PREFETCH");
     if (const char* v = std::getenv("FFTSPLIT_CONTRACT_TILE")) {
         if (*v) {
+            plan->con_prefetch = 2;
             int prod = 4;
             const char* q = v;
             if (!std::strncmp(q, "g3:", 3)) { prod = 3; q += 3; }
@@ -334,15 +344,21 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
             plan->con_products = prod;
         }
     }
-    // the LDS-prefetch variants exist for the 3-product 64x64, 128x32,
-    // 128x64 and 64x128 tiles with 16-channel stages (three stages ahead
-    // for 64x64 only)
+    if (pf_env) {
+        const int pf = std::atoi(pf_env);
+        if (pf >= 1 && pf <= 3) plan->con_prefetch = pf;
+    }
+    // the LDS-prefetch variants exist for the 3-product tiles with
+    // 16-channel stages (64x64, 128x32, 128x64, 64x128; three stages ahead
+    // for 64x64 only) and for 64x64 with 8-channel stages
     {
-        const bool lds_variant = plan->con_products == 3 && plan->con_kc == 16 &&
-                                 ((plan->con_bm == 64 && plan->con_bn == 64) ||
-                                  (plan->con_bm == 128 && plan->con_bn == 32) ||
-                                  (plan->con_bm == 128 && plan->con_bn == 64) ||
-                                  (plan->con_bm == 64 && plan->con_bn == 128));
+        const bool t64 = plan->con_bm == 64 && plan->con_bn == 64;
+        const bool lds_variant =
+            plan->con_products == 3 &&
+            ((plan->con_kc == 16 && (t64 || (plan->con_bm == 128 && plan->con_bn == 32) ||
+                                     (plan->con_bm == 128 && plan->con_bn == 64) ||
+                                     (plan->con_bm == 64 && plan->con_bn == 128))) ||
+             (plan->con_kc == 8 && t64));
         if (!lds_variant) plan->con_prefetch = 1;
         if (plan->con_prefetch == 3 && plan->con_bm != 64) plan->con_prefetch = 2;
     }

@@ -285,6 +285,34 @@ def test_contraction_prefetch_choice(monkeypatch):
     assert plan(n=32, cin=512, h=14, w=14, cout=512, k=3, tile=14).info.contract_prefetch == 2
 
 
+def test_contraction_stage_choice(monkeypatch):
+    """8-channel stages three ahead where a layer has at most 128 input
+    channels and at least 8192 64 x 64 workgroups (the VGG-16 layers at 224^2
+    and 112^2); 16-channel stages two ahead elsewhere; a tile override
+    restores the two-ahead default, and the prefetch override still applies."""
+    monkeypatch.delenv("FFTSPLIT_CONTRACT_PREFETCH", raising=False)
+    monkeypatch.delenv("FFTSPLIT_CONTRACT_TILE", raising=False)
+    def choice(**kw):
+        i = plan(**kw).info
+        return (i.contract_tile_m, i.contract_tile_n, i.contract_stage_k, i.contract_prefetch)
+    assert choice(n=32, cin=64, h=224, w=224, cout=64, k=3, tile=14) == (64, 64, 8, 3)
+    assert choice(n=32, cin=64, h=112, w=112, cout=128, k=3, tile=14) == (64, 64, 8, 3)
+    assert choice(n=32, cin=128, h=112, w=112, cout=128, k=3, tile=14) == (64, 64, 8, 3)
+    assert choice(n=32, cin=128, h=56, w=56, cout=256, k=3, tile=14) == (64, 64, 16, 2)   # 4096 workgroups
+    assert choice(n=32, cin=256, h=56, w=56, cout=256, k=3, tile=14) == (64, 64, 16, 2)
+    assert choice(n=1, cin=64, h=224, w=224, cout=64, k=3, tile=14) == (64, 64, 16, 2)
+    assert choice(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28) == (64, 64, 16, 2)
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", "g3:64x64x16")
+    assert choice(n=32, cin=64, h=224, w=224, cout=64, k=3, tile=14) == (64, 64, 16, 2)
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", "g3:64x64x8")
+    assert choice(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28) == (64, 64, 8, 2)
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_PREFETCH", "3")
+    assert choice(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28) == (64, 64, 8, 3)
+    monkeypatch.delenv("FFTSPLIT_CONTRACT_TILE")
+    monkeypatch.setenv("FFTSPLIT_CONTRACT_PREFETCH", "1")
+    assert choice(n=32, cin=64, h=224, w=224, cout=64, k=3, tile=14) == (64, 64, 8, 1)
+
+
 @pytest.mark.parametrize("value", ["0x0x0", "-64x64x16", "g3:64x64x32", "g3:256x64x16", "64x64x16junk",
                                    "64x64", "g5:64x64x16", "96x64x16"])
 def test_contraction_tile_override_is_validated(value, monkeypatch):

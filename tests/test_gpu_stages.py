@@ -189,6 +189,40 @@ def test_contraction_stage_pipeline(cin, cout, prefetch, monkeypatch):
     assert np.array_equal(plan1.yspec_view(ws1).cpu().numpy(), Y)
 
 
+@pytest.mark.parametrize("cin", [8, 20, 40, 64, 100])
+def test_contraction_eight_channel_stages(cin, monkeypatch):
+    """The 64 x 64 tile with 8-channel stages (the plan's choice for few
+    input channels and many workgroups), loaded one, two and three stages
+    ahead, partial last stages included: against the oracle's channel sum,
+    and equal to the 16-channel stages' result (the same products added in
+    the same channel order)."""
+    shape = (2, cin, 24, 24, 64, 3)
+    x, wt = small_layer(*shape, seed=100 + cin)
+    outs = []
+    for tile_env, pf in (("g3:64x64x16", "2"), ("g3:64x64x8", "1"), ("g3:64x64x8", "2"), ("g3:64x64x8", "3")):
+        monkeypatch.setenv("FFTSPLIT_CONTRACT_TILE", tile_env)
+        monkeypatch.setenv("FFTSPLIT_CONTRACT_PREFETCH", pf)
+        plan = fs.Plan(*shape, tile=14)
+        info = plan.info
+        assert (info.contract_tile_m, info.contract_tile_n, info.contract_prefetch) == (64, 64, int(pf))
+        print(f"[case] cin={cin} {tile_env} prefetch={pf}", flush=True)
+        ws = plan.new_workspace()
+        wspec = plan.transform_weights(_dev(wt))
+        plan.forward(_dev(x), ws)
+        plan.contract(wspec, ws)
+        torch.cuda.synchronize()
+        outs.append(plan.yspec_view(ws).cpu().numpy())
+    X = plan.xspec_view(ws).cpu().numpy().astype(np.complex128)
+    W = plan.wspec_view(wspec).cpu().numpy().astype(np.complex128)
+    ref = oracle.hadamard_channel_sum(X.transpose(2, 1, 0), np.conj(W).transpose(2, 1, 0)).transpose(2, 1, 0)
+    for f in (-2, -1):
+        ref[f] = (np.einsum("ic,it->ct", W[f].real, X[f].real)
+                  + 1j * np.einsum("ic,it->ct", W[f].imag, X[f].imag))
+    for o in outs:
+        assert rel_l2(o, ref) < 2e-6
+        assert np.array_equal(o, outs[0])
+
+
 @pytest.mark.parametrize("tile_env,n", [("g3:128x64x16", 16), ("g3:64x128x16", 32)])
 def test_contraction_other_tiles(tile_env, n, monkeypatch):
     """The 128 x 64 and 64 x 128 tiles (plan options), both prefetch depths,

@@ -26,6 +26,8 @@ BUDGETS = [
     # three 48 KB workgroups of four waves per CU: three waves per SIMD
     ("k_contract.o", r"contract_kernelILi64ELi64ELi16ELi2ELb1ELi2E", 168),
     ("k_contract.o", r"contract_kernelILi128ELi32ELi16ELi4ELb1ELi2E", 168),
+    # 8-channel stages three ahead: four 32 KB workgroups per CU, four waves per SIMD
+    ("k_contract.o", r"contract_kernelILi64ELi64ELi8ELi2ELb1ELi3E", 128),
     # four 128-thread workgroups (L = 32) or two 256-thread ones: two waves per SIMD
     ("k_forward.o", r"forward_band_kernelILi32ELi8ELi16E", 256),
     ("k_forward.o", r"forward_band_kernelILi16ELi32ELi8E", 128),
