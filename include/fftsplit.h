@@ -152,8 +152,10 @@ typedef struct {
      * fftsplit_direct_transform_weights. */
     size_t direct_wspec_bytes;
     /* Input-channel stages the contraction loads ahead of the one it
-     * multiplies: 1 (through registers) or 2 (straight into LDS, the
-     * default where the tile has that variant).  The environment variable
+     * multiplies: 1 (through registers), or 2 or 3 straight into LDS (2 the
+     * default where the tile has that variant, 3 with the 8-channel stages
+     * the plan picks for layers of at most 128 input channels and at least
+     * 8192 workgroups).  The environment variable
      * FFTSPLIT_CONTRACT_PREFETCH=1..3 overrides it at plan time. */
     int contract_prefetch;
     /* The plan's cost model for the chosen L (Section 3.2 weighs the
