@@ -189,7 +189,7 @@ def test_contraction_stage_pipeline(cin, cout, prefetch, monkeypatch):
     assert np.array_equal(plan1.yspec_view(ws1).cpu().numpy(), Y)
 
 
-@pytest.mark.parametrize("cin", [8, 20, 40, 64, 100])
+@pytest.mark.parametrize("cin", [4, 8, 12, 20, 40, 64, 100])
 def test_contraction_eight_channel_stages(cin, monkeypatch):
     """The 64 x 64 tile with 8-channel stages (the plan's choice for few
     input channels and many workgroups), loaded one, two and three stages
