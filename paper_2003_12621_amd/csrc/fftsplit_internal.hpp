@@ -36,9 +36,10 @@ struct fftsplit_plan_s {
     // inv_band; LDS pitch of the output band and dynamic LDS bytes
     bool inv_band;
     int inv_obp, inv_lds;
-    // FFTSPLIT_MAXPOOL: pooled inside the band inverse's store phase if
-    // pool_fused, else the inverse writes the unpooled output to the
-    // workspace at pre_off and a pooling pass follows
+    // FFTSPLIT_MAXPOOL: pooled inside the overlap-save inverse's store
+    // phase (band or general kernel) if pool_fused, else the inverse writes
+    // the unpooled output to the workspace at pre_off and a pooling pass
+    // follows
     bool pool_fused;
     size_t pre_off, pre_bytes;
     // inputs of at most 4 (L = 8) or 3 (L = 16) channels (overlap-save,

@@ -54,7 +54,7 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
                                                                const float* __restrict__ bias, float* __restrict__ y,
                                                                float* __restrict__ aux, int cout, int coutp, int h,
                                                                int w, int T, int P, int th, int tw, int nt, int ntp,
-                                                               int ngroups, int relu, int y_elems) {
+                                                               int ngroups, int relu, int pool, int y_elems) {
     using S = InvShape<L, TG>;
     constexpr int H2 = S::H2, NT = S::NT, TP = S::TP, TTS = S::TTS, SP = S::SP, STS = S::STS;
     extern __shared__ float4 lds_raw[];
@@ -81,7 +81,10 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
             // overlap-add: rows/cols of the core (offset P) inside the image.
             ro = OAA ? min(T - 2 * P, h - a * T - P) : min(T, h - a * T);
             cw = OAA ? min(T - 2 * P, w - b * T - P) : min(T, w - b * T);
-            off = ((img * cout + co) * h + a * T) * w + b * T + (OAA ? P * w + P : 0);
+            // pool (overlap-save, T even): the tile's pooled origin in the
+            // [h/2][w/2] output
+            off = pool ? ((img * cout + co) * (h >> 1) + ((a * T) >> 1)) * (w >> 1) + ((b * T) >> 1)
+                       : ((img * cout + co) * h + a * T) * w + b * T + (OAA ? P * w + P : 0);
         }
         dst_off[tid] = off;
         rows_ok[tid] = ro;
@@ -183,7 +186,23 @@ __global__ __launch_bounds__(TG * (L / 2)) void inverse_kernel(const float2* __r
             const int ro = rows_ok[u], cw = cols_ok[u];
             const int d = dst_off[u];
             const float* s = st + u * STS;
-            if (!OAA) {
+            if (!OAA && pool) {
+                // 2x2 max-pool of the crop (T is even, so no pooling window
+                // straddles two patches; floor at an odd image edge), then
+                // bias and ReLU, which commute with the maximum; lane q < L/2
+                // takes pooled column q of pooled rows m
+                const int qq = q < L / 2 ? q : 0;
+                const unsigned vq = unsigned(d + q) * 4u;
+#pragma unroll
+                for (int mb = 0; mb < L / 2; mb += S::MS) {
+                    const int m = mb + ms;
+                    const float* sp = s + 2 * m * SP + 2 * qq;
+                    float v = vmax(vmax3(sp[0], sp[1], sp[SP]), sp[SP + 1]) + bv;
+                    if (relu) v = vmax(v, 0.f);
+                    const bool in = m < (ro >> 1) && q < (cw >> 1);
+                    buf_store_f32(v, ry_out, in ? vq + unsigned(m * (w >> 1)) * 4u : kOutOfRange, 0);
+                }
+            } else if (!OAA) {
                 // Output through a descriptor over y: lanes outside the crop
                 // (m >= ro or q >= cw) get an out-of-range offset, which drops
                 // the store.
@@ -938,9 +957,12 @@ static hipError_t launch_inverse_v(const fftsplit_plan_s& p, const float2* ys, c
     if (attr != hipSuccess) return attr;
     const int ngroups = p.ntp / TG;
     const dim3 grid(unsigned(ngroups) * unsigned(p.prob.cout));
+    const bool pool = !OAA && p.pool_fused;
+    const int y_elems = pool ? p.prob.n * p.prob.cout * (p.prob.h / 2) * (p.prob.w / 2)
+                             : p.prob.n * p.prob.cout * p.prob.h * p.prob.w;
     hipError_t e = launch_kernel(kern, grid, dim3(S::NT), S::LDS_BYTES, s, ev.start, OAA ? nullptr : ev.stop, ys,
                                  bias, y, aux, p.prob.cout, p.coutp, p.prob.h, p.prob.w, p.T, p.P, p.th, p.tw, p.nt,
-                                 p.ntp, ngroups, int(p.relu), p.prob.n * p.prob.cout * p.prob.h * p.prob.w);
+                                 p.ntp, ngroups, int(p.relu), int(pool), y_elems);
     if (e != hipSuccess || !OAA) return e;
     return launch_seam(p, aux, bias, y, s, ev.stop);
 }

@@ -371,10 +371,12 @@ static fftsplit_status_t build_plan(const fftsplit_problem_t* prob, int device, 
 
     choose_forward_band(*plan);
     choose_inverse_band(*plan);
-    // The max-pool goes into the band inverse's store phase when its slots
-    // pair up into pooled rows (even tile size, even image height);
-    // otherwise the unpooled output is staged in the workspace.
-    plan->pool_fused = pool && plan->inv_band && g.T % 2 == 0 && p.h % 2 == 0;
+    // The max-pool goes into the overlap-save inverse's store phase when no
+    // pooling window straddles two tiles (even tile size) and, for the band
+    // inverse, its slots pair up into pooled rows (even image height);
+    // otherwise the unpooled output is staged in the workspace and pooled
+    // by a separate pass.
+    plan->pool_fused = pool && !oaa && g.L % 2 == 0 && g.T % 2 == 0 && (!plan->inv_band || p.h % 2 == 0);
     // Layers with at most 4 (L = 8) or 3 (L = 16) input channels, whose
     // patch spectra fit the inverse's registers: the channel sum moves into
     // the inverse (no contraction launch, output spectra never stored).

@@ -208,7 +208,12 @@ POOL_CASES = [
     ((3, 4, 56, 56, 70, 5), 28, "os"),    # band, items spanning images
     ((1, 3, 60, 40, 6, 3), 6, "os"),      # band, T/2 odd and items starting mid tile-row: straddles
     ((2, 3, 26, 44, 5, 3), 14, "os"),     # band, ragged last tile rows and columns
-    ((1, 2, 27, 28, 4, 3), 14, "os"),     # odd height: staged output + pooling pass
+    ((1, 2, 27, 28, 4, 3), 14, "os"),     # band, odd height: staged output + pooling pass
+    ((3, 6, 14, 14, 7, 3), 14, "os"),     # general inverse (width 14), pooled in its store phase
+    ((2, 3, 30, 26, 5, 3), 14, "os"),     # general, ragged last tiles
+    ((1, 2, 27, 30, 4, 3), 6, "os"),      # general, L = 8, odd height: floor in the store phase
+    ((2, 3, 22, 18, 5, 5), 12, "os"),     # general, K = 5
+    ((1, 2, 21, 34, 3, 3), 30, "os"),     # general, L = 32, one partial tile per row
     ((1, 3, 30, 30, 5, 3), 14, "oaa"),    # overlap-add: staged output + pooling pass
     ((2, 3, 17, 19, 4, 3), 3, "oaa"),     # OaAConv configuration, odd sizes
 ]
