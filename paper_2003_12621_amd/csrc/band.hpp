@@ -64,7 +64,7 @@ struct PairRole {
     static constexpr int P = TG / 2, Q = P < 8 ? P : 8, CPW = 64 / TG;
     static_assert(TG <= 32 && TG % 2 == 0, "patch pairs need work items of at most 32 patches");
     int pm, hi, patch, col;
-    __device__ PairRole(int lane, int wave) {
+    __host__ __device__ PairRole(int lane, int wave) {
         const int r = lane & 31, s = r / Q;
         hi = lane >> 5;
         pm = (s / CPW) * Q + r % Q;
