@@ -572,18 +572,28 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void inverse_band_kernel(
                 return k == 0 ? make_float2(pb[0].x, 0.f) : (k == H2 ? make_float2(pb[0].y, 0.f) : pb[k]);
             };
             float2 cz[L];
+            // Only the first wave has a lane j = 0.  At L = 16 the other
+            // waves skip the Hermitian rebuild and its selects (a branch on
+            // the wave index, the same in every lane of a wave); at L = 32
+            // that branch made the inverse slower, so every wave runs the
+            // selects there.
+            if (L != 16 || wv == 0) {
 #pragma unroll
-            for (int k1 = 0; k1 < L; ++k1) {
-                float2 v0;
-                if (k1 <= H2) {  // lane 0: U = Y0 + i YH
-                    const float2 a = y0(k1), b = yh(k1);
-                    v0 = make_float2(a.x - b.y, a.y + b.x);
-                } else {         // lane 0: Y0[k1] = conj(Y0[L-k1]), likewise YH
-                    const float2 a = y0(L - k1), b = yh(L - k1);
-                    v0 = make_float2(a.x + b.y, b.x - a.y);
+                for (int k1 = 0; k1 < L; ++k1) {
+                    float2 v0;
+                    if (k1 <= H2) {  // lane 0: U = Y0 + i YH
+                        const float2 a = y0(k1), b = yh(k1);
+                        v0 = make_float2(a.x - b.y, a.y + b.x);
+                    } else {         // lane 0: Y0[k1] = conj(Y0[L-k1]), likewise YH
+                        const float2 a = y0(L - k1), b = yh(L - k1);
+                        v0 = make_float2(a.x + b.y, b.x - a.y);
+                    }
+                    const float2 v1 = k1 < H2 ? pa[k1] : pb[k1 - H2];
+                    cz[k1] = j0 ? v0 : v1;
                 }
-                const float2 v1 = k1 < H2 ? pa[k1] : pb[k1 - H2];
-                cz[k1] = j0 ? v0 : v1;
+            } else {
+#pragma unroll
+                for (int k1 = 0; k1 < L; ++k1) cz[k1] = k1 < H2 ? pa[k1] : pb[k1 - H2];
             }
             // NCI > 0: the next item's filter spectra stay in flight
             // through this whole item
