@@ -14,7 +14,9 @@
 //   3. overlap-save placement: the top-left T x T block of each patch is its
 //      output tile (the crop), staged in LDS and written back row by row
 //      with bias and ReLU; horizontally adjacent patches of a group land in
-//      one contiguous run of the output row (the concatenation).
+//      one contiguous run of the output row (the concatenation).  With the
+//      fused max-pool (T even) each 2x2 block of the staged crop is reduced
+//      to its maximum first and the [h/2][w/2] output written instead;
 //   3'. overlap-add placement (zero-padded patches): entry (p, q) of a
 //      patch's L x L result belongs at output (aT+P+p', bT+P+q') with
 //      p' = p for p < T and p - L otherwise, so each patch covers the L x L
