@@ -31,7 +31,10 @@
 // stage the operand fragments of the next channel pair are read from LDS
 // while the current pair's MFMAs run.  The filter spectra, the bulk of the
 // bytes, are loaded non-temporally where each block of them is read by one
-// workgroup, so they do not evict the patch and output spectra.  The
+// workgroup, so they do not evict the patch and output spectra; with XS (a
+// single 64-channel output block, so every patch spectrum is read by one
+// workgroup) the patch spectra are too, so that they do not evict the
+// output spectra the inverse reads next.  The
 // workgroups of one bin run on the same XCD, so the bin's patch spectra
 // are fetched from HBM once and reused from L2, and the bins are dealt to
 // the XCDs in turn, so that together they sweep the spectra in order.
@@ -182,7 +185,7 @@ __device__ __forceinline__ void multiply_stage(const float2* stage, floatx16 (&a
     }
 }
 
-template <int BM, int BN, int KC, int WM, bool G3, int PF>
+template <int BM, int BN, int KC, int WM, bool G3, int PF, bool XS>
 __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict__ xs, const float2* __restrict__ ws,
                                                        float2* __restrict__ ys, int cin, int coutp, int ntp,
                                                        int nbco, int nbt, int nbins, int ygroup, int npacked) {
@@ -348,7 +351,7 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
             for (int i = 0; i < S::XL; ++i) {
                 const int e = i * S::NT + tid;
                 const uint4* g = reinterpret_cast<const uint4*>(xrow(k0 + e / (BN / 2))) + e % (BN / 2);
-                lds_dma16<false>(g, sx + i * S::NT + wbase);
+                lds_dma16<XS>(g, sx + i * S::NT + wbase);
             }
         };
         // full stage s in buffer `cur`; stage s + PF goes into `ahead` (the
@@ -389,11 +392,11 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
                                   ntp, krow, col, packed);
 }
 
-template <int BM, int BN, int KC, int WM, bool G3 = false, int PF = 1>
+template <int BM, int BN, int KC, int WM, bool G3 = false, int PF = 1, bool XS = false>
 static hipError_t launch_contract_v(const fftsplit_plan_s& p, const float2* xs, const float2* ws, float2* ys,
                                     hipStream_t s, const LaunchEvents& ev) {
     using S = ConShape<BM, BN, KC, WM>;
-    auto kern = contract_kernel<BM, BN, KC, WM, G3, PF>;
+    auto kern = contract_kernel<BM, BN, KC, WM, G3, PF, XS>;
     constexpr int lds = (PF > 1 ? PF + 1 : 2) * (S::WE + S::XE) * 8;
     static hipError_t attr = allow_dynamic_lds(kern, lds);
     if (attr != hipSuccess) return attr;
@@ -422,10 +425,14 @@ hipError_t launch_contract(const fftsplit_plan_s& p, const float2* xs, const flo
     if (p.con_products == 3) {
         switch (v) {
             case 64064016:
+                if (p.con_prefetch == 2 && p.coutp == 64)
+                    return launch_contract_v<64, 64, 16, 2, true, 2, true>(p, xs, ws, ys, s, ev);
                 if (p.con_prefetch == 2) return launch_contract_v<64, 64, 16, 2, true, 2>(p, xs, ws, ys, s, ev);
                 if (p.con_prefetch == 3) return launch_contract_v<64, 64, 16, 2, true, 3>(p, xs, ws, ys, s, ev);
                 return launch_contract_v<64, 64, 16, 2, true>(p, xs, ws, ys, s, ev);
             case 64064008:
+                if (p.con_prefetch == 3 && p.coutp == 64)
+                    return launch_contract_v<64, 64, 8, 2, true, 3, true>(p, xs, ws, ys, s, ev);
                 if (p.con_prefetch == 3) return launch_contract_v<64, 64, 8, 2, true, 3>(p, xs, ws, ys, s, ev);
                 if (p.con_prefetch == 2) return launch_contract_v<64, 64, 8, 2, true, 2>(p, xs, ws, ys, s, ev);
                 return launch_contract_v<64, 64, 8, 2, true>(p, xs, ws, ys, s, ev);
