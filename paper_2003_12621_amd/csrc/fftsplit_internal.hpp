@@ -29,8 +29,9 @@ struct fftsplit_plan_s {
     // overlap-save band variant of the forward transform (band.hpp):
     // used if fwd_band; LDS row pitch, left zero columns, zero-row slot and
     // dynamic LDS bytes; fwd_sweep: items a grid apart instead of a
-    // contiguous run per workgroup
-    bool fwd_band, fwd_sweep;
+    // contiguous run per workgroup; fwd_stream: the input read
+    // non-temporally
+    bool fwd_band, fwd_sweep, fwd_stream;
     int fwd_bp, fwd_co, fwd_zslot, fwd_lds;
     // overlap-save band variant of the inverse transform: used if
     // inv_band; LDS pitch of the output band and dynamic LDS bytes

@@ -222,7 +222,10 @@ __global__ __launch_bounds__(TG * (L / 2)) void forward_kernel(const float* __re
 //     stores of neighbouring items overlap; `sweep` (set by the plan where
 //     input and spectra exceed the last-level cache) spaces a workgroup's
 //     items a grid apart, so the workgroups sweep input and spectra in
-//     order, otherwise a workgroup runs a contiguous run of items;
+//     order, otherwise a workgroup runs a contiguous run of items; with XS
+//     (an input larger than the last-level cache) the input is read
+//     non-temporally, so that it does not take the cache's room from the
+//     spectra the contraction reads next;
 //   * LDS banks (32 four-byte banks): the row pass pairs rows j and
 //     j + L/2 (not 2j and 2j+1); with the odd band pitch the L/2 row-pass
 //     lanes of a patch, which read rows j, hit distinct banks, and with the
@@ -231,7 +234,7 @@ __global__ __launch_bounds__(TG * (L / 2)) void forward_kernel(const float* __re
 //     the column-pass reads of the patches and columns that share a bank
 //     sweep in distinct banks; the band is written with 4-byte stores (odd
 //     rows are not 8-byte aligned).
-template <int L, int TG, int NV>
+template <int L, int TG, int NV, bool XS>
 __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
     const float* __restrict__ x, float2* __restrict__ xs, int cin, int h, int w, int T, int P, int th, int tw, int nt,
     int ntp, int ngroups, int nitems, int ipw, int bp, int co, int zslot, unsigned x_bytes, float inv_h, float inv_tw,
@@ -302,7 +305,8 @@ __global__ __launch_bounds__(TG * (L / 2), 2) void forward_band_kernel(
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
             const bool ok = lane_ok && sl0 + k * slot_step < g.slots;
-            v[k] = buf_load_f32x4(rxin, ok ? voff : kOutOfRange, unsigned(k * slot_step * w * 4));
+            v[k] = buf_load_f32x4<XS ? kCacheStream : kCacheDefault>(rxin, ok ? voff : kOutOfRange,
+                                                                     unsigned(k * slot_step * w * 4));
             r += dr;
             voff += dq_off;
             const bool carry = r >= h;
@@ -464,11 +468,11 @@ static hipError_t launch_forward_L(const fftsplit_plan_s& p, const float* x, flo
     return p.oaa ? launch_forward_v<L, TG, true>(p, x, xs, s, ev) : launch_forward_v<L, TG, false>(p, x, xs, s, ev);
 }
 
-template <int L, int TG, int NV>
-static hipError_t launch_forward_band(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s,
+template <int L, int TG, int NV, bool XS>
+static hipError_t launch_forward_band_v(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s,
                                       const LaunchEvents& ev) {
     using S = FwdShape<L, TG>;
-    auto kern = forward_band_kernel<L, TG, NV>;
+    auto kern = forward_band_kernel<L, TG, NV, XS>;
     const int lds = p.fwd_lds;
     if (lds > 64 * 1024) {
         const hipError_t attr = allow_dynamic_lds(kern, lds);
@@ -488,6 +492,16 @@ static hipError_t launch_forward_band(const fftsplit_plan_s& p, const float* x, 
                          p.prob.w, p.T, p.P, p.th, p.tw, p.nt, p.ntp, ngroups, nitems, ipw, p.fwd_bp, p.fwd_co,
                          p.fwd_zslot, x_bytes, 1.0f / float(p.prob.h), 1.0f / float(p.tw), 1.0f / float(p.th),
                          p.fwd_sweep ? 1 : 0);
+}
+
+// XS where the input exceeds the last-level cache (plan fwd_stream): the
+// input is read non-temporally, so that it does not evict the spectra the
+// contraction reads next.
+template <int L, int TG, int NV>
+static hipError_t launch_forward_band(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s,
+                                      const LaunchEvents& ev) {
+    return p.fwd_stream ? launch_forward_band_v<L, TG, NV, true>(p, x, xs, s, ev)
+                       : launch_forward_band_v<L, TG, NV, false>(p, x, xs, s, ev);
 }
 
 hipError_t launch_forward(const fftsplit_plan_s& p, const float* x, float2* xs, hipStream_t s,
