@@ -31,7 +31,7 @@
 // stage the operand fragments of the next channel pair are read from LDS
 // while the current pair's MFMAs run.  The filter spectra, the bulk of the
 // bytes, are loaded non-temporally where each block of them is read by one
-// workgroup, so they do not evict the patch and output spectra; with XS (a
+// or two workgroups, so they do not evict the patch and output spectra; with XS (a
 // single 64-channel output block, so every patch spectrum is read by one
 // workgroup) the patch spectra are too, so that they do not evict the
 // output spectra the inverse reads next.  The
@@ -224,10 +224,12 @@ __global__ __launch_bounds__(256) void contract_kernel(const float2* __restrict_
 
     const float4* wsrc = reinterpret_cast<const float4*>(ws + size_t(f) * cin * coutp + co0);
     // The filter spectra are streamed (non-temporal) when each block of them
-    // is read by one workgroup only (one patch block per bin); with several
-    // patch blocks per bin every workgroup of the bin reads the same block,
-    // which then has to stay in the caches.
-    const bool w_once = nbt == 1;
+    // is read by at most two workgroups (one or two patch blocks per bin):
+    // the two run side by side on the bin's XCD, so the second still finds
+    // the block in L2, and the last-level cache is spared the stream (VGG-16
+    // layers at 28^2, 128 patches: up to 6 us each).  With more patch
+    // blocks per bin the block has to stay in the caches.
+    const bool w_once = nbt <= 2;
     const int wrow4 = coutp / 2;   // row pitch in float4
     // Patch spectra are channel-blocked (fftsplit.h): input channel ci of
     // bin f starts at spec_offset(ci, f, 0); within a block of 16 channels
