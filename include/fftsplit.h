@@ -177,6 +177,9 @@ typedef struct {
      * input and the patch spectra together exceed 256 MB;
      * FFTSPLIT_FORWARD_SWEEP=1 / 0 forces it at plan time). */
     int forward_band, forward_sweep, inverse_band;
+    /* 1 if the row-band forward reads its input non-temporally (an input
+     * larger than the 256 MB last-level cache). */
+    int forward_stream;
 } fftsplit_plan_info_t;
 
 /* Validate `prob` (host) and create a plan for `device` (a HIP ordinal).

@@ -61,7 +61,8 @@ class PlanInfo(ctypes.Structure):
                 ("direct_wspec_bytes", ctypes.c_size_t), ("contract_prefetch", ctypes.c_int),
                 ("model_contract_flops", ctypes.c_double), ("model_transform_bytes", ctypes.c_double),
                 ("model_seconds", ctypes.c_double),
-                ("forward_band", ctypes.c_int), ("forward_sweep", ctypes.c_int), ("inverse_band", ctypes.c_int)]
+                ("forward_band", ctypes.c_int), ("forward_sweep", ctypes.c_int), ("inverse_band", ctypes.c_int),
+                ("forward_stream", ctypes.c_int)]
 
 
 class FftsplitError(RuntimeError):

@@ -460,6 +460,7 @@ FFTSPLIT_EXPORT fftsplit_status_t fftsplit_plan_info(fftsplit_plan_t plan, fftsp
     i.forward_band = plan->fwd_band ? 1 : 0;
     i.forward_sweep = plan->fwd_band && plan->fwd_sweep ? 1 : 0;
     i.inverse_band = plan->inv_band ? 1 : 0;
+    i.forward_stream = plan->fwd_band && plan->fwd_stream ? 1 : 0;
     i.model_contract_flops = plan->model_con_flops;
     i.model_transform_bytes = plan->model_xfer_bytes;
     i.model_seconds = plan->model_seconds;

@@ -371,13 +371,18 @@ def test_transform_variant_choice(monkeypatch):
     """Row-band transforms where the width allows them; the forward's items
     a grid apart only where input and patch spectra exceed 256 MB (the
     VGG-16 layer 2 at batch 32: 411 + 537 MB), contiguous runs otherwise;
-    the environment forces either."""
+    the environment forces either.  The input read non-temporally only
+    where it alone exceeds 256 MB (layer 2's 411 MB; not layer 4's 205 MB,
+    whose items are swept too)."""
     big = plan(n=32, cin=64, h=224, w=224, cout=64, k=3, tile=14).info
     assert (big.forward_band, big.forward_sweep, big.inverse_band) == (1, 1, 1)
     k5 = plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info
     assert (k5.forward_band, k5.forward_sweep, k5.inverse_band) == (1, 0, 1)
     narrow = plan(n=32, cin=512, h=14, w=14, cout=512, k=3, tile=14).info   # width not a multiple of 4
     assert (narrow.forward_band, narrow.forward_sweep, narrow.inverse_band) == (0, 0, 0)
+    assert (big.forward_stream, k5.forward_stream, narrow.forward_stream) == (1, 0, 0)
+    l4 = plan(n=32, cin=128, h=112, w=112, cout=128, k=3, tile=14).info
+    assert (l4.forward_sweep, l4.forward_stream) == (1, 0)
     monkeypatch.setenv("FFTSPLIT_FORWARD_SWEEP", "1")
     assert plan(n=16, cin=256, h=56, w=56, cout=256, k=5, tile=28).info.forward_sweep == 1
     monkeypatch.setenv("FFTSPLIT_FORWARD_SWEEP", "0")
